@@ -1,0 +1,280 @@
+// C-ABI front end: argument validation (before any launch, no side effects),
+// workspace layout, and the launch sequence of each entry point.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "dora_internal.h"
+
+using namespace dora;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool geometry_supported(const dora_decode_desc& d) {
+  if (d.head_dim != 64 && d.head_dim != 128) return false;
+  if (d.page_size != 16 && d.page_size != 32) return false;
+  if (d.kv_dtype != DORA_KV_BF16 && d.kv_dtype != DORA_KV_FP8_E4M3) return false;
+  const int G = d.num_q_heads / d.num_kv_heads;
+  return G >= 1 && G <= 16;
+}
+
+// Host-checkable validity of a descriptor (pointers are checked separately).
+dora_status check_desc(const dora_decode_desc* d) {
+  if (!d) return DORA_ERR_INVALID_ARG;
+  if (d->num_seqs < 0 || d->num_kv_heads < 1 || d->num_q_heads < 1 ||
+      d->num_q_heads % d->num_kv_heads != 0 || d->block_table_stride < 1 ||
+      d->num_pages < 1 || d->head_dim < 1 || d->page_size < 1 || !(d->sm_scale >= 0.f) ||
+      d->target_units < 0 || (d->flags & ~(DORA_FLAG_VALIDATE | DORA_FLAG_FORCE_SPLIT)) != 0)
+    return DORA_ERR_INVALID_ARG;
+  if ((d->flags & DORA_FLAG_FORCE_SPLIT) && d->split_pages < 1) return DORA_ERR_INVALID_ARG;
+  if (!geometry_supported(*d)) return DORA_ERR_UNSUPPORTED;
+  return DORA_OK;
+}
+
+int target_units_of(const dora_decode_desc& d) {
+  return d.target_units > 0 ? d.target_units : kDefaultTargetUnits;
+}
+
+}  // namespace
+
+namespace dora {
+
+bool ws_layout(const dora_decode_desc& d, WsLayout* out) {
+  const int64_t B = d.num_seqs;
+  const int64_t Hkv = d.num_kv_heads;
+  const int64_t G = d.num_q_heads / d.num_kv_heads;
+  int64_t items;
+  if (d.flags & DORA_FLAG_FORCE_SPLIT) {
+    // every sequence holds at most block_table_stride pages
+    items = B * ((d.block_table_stride + d.split_pages - 1) / d.split_pages);
+  } else {
+    // sum_b max(1, ceil(n_b / C)) <= total / C + B <= target / Hkv + B
+    const int64_t tu = target_units_of(d);
+    items = (tu + Hkv - 1) / Hkv + B;
+  }
+  if (items < 1) items = 1;
+  WsLayout w;
+  w.max_items = items;
+  size_t off = kWsHeaderBytes;
+  w.seqinfo_off = off;
+  off = align_up(off + (size_t)B * 8);
+  w.items_off = off;
+  off = align_up(off + (size_t)items * 16);
+  w.part_o_off = off;
+  off = align_up(off + (size_t)items * Hkv * G * d.head_dim * 4);
+  w.part_ml_off = off;
+  off = align_up(off + (size_t)items * Hkv * G * 8);
+  w.total = off;
+  *out = w;
+  return true;
+}
+
+}  // namespace dora
+
+extern "C" {
+
+const char* dora_status_string(dora_status s) {
+  switch (s) {
+    case DORA_OK: return "ok";
+    case DORA_ERR_INVALID_ARG: return "invalid argument";
+    case DORA_ERR_UNSUPPORTED: return "unsupported geometry or dtype";
+    case DORA_ERR_WORKSPACE_TOO_SMALL: return "workspace or buffer too small";
+    case DORA_ERR_VERSION_MISMATCH: return "policy version mismatch";
+    case DORA_ERR_POOL_EXHAUSTED: return "page pool exhausted";
+    case DORA_ERR_DEVICE_CHECK: return "device data check failed";
+    case DORA_ERR_HIP: return "HIP runtime error";
+    case DORA_ERR_NOT_FOUND: return "sequence not found";
+  }
+  return "unknown status";
+}
+
+size_t dora_decode_workspace_bytes(const dora_decode_desc* desc) {
+  if (check_desc(desc) != DORA_OK) return 0;
+  WsLayout w;
+  if (!ws_layout(*desc, &w)) return 0;
+  return w.total;
+}
+
+dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const void* k_pages,
+                             const void* v_pages, const int32_t* block_table,
+                             const int32_t* seq_lens, const int32_t* version_ids, void* out,
+                             void* workspace, size_t workspace_bytes, dora_stream_t stream) {
+  dora_status st = check_desc(desc);
+  if (st != DORA_OK) return st;
+  const dora_decode_desc& d = *desc;
+  if (d.num_seqs == 0) return DORA_OK;
+  const bool fp8 = d.kv_dtype == DORA_KV_FP8_E4M3;
+  const bool validate = (d.flags & DORA_FLAG_VALIDATE) != 0;
+  if (!q || !k_pages || !v_pages || !block_table || !seq_lens || !out || !workspace)
+    return DORA_ERR_INVALID_ARG;
+  if (fp8 && (!d.k_scales || !d.v_scales)) return DORA_ERR_INVALID_ARG;
+  if (validate && (!version_ids && d.page_owner)) return DORA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k_pages) || !aligned16(v_pages) || !aligned16(out) ||
+      !aligned16(workspace))
+    return DORA_ERR_INVALID_ARG;
+  WsLayout w;
+  ws_layout(d, &w);
+  if (workspace_bytes < w.total) return DORA_ERR_WORKSPACE_TOO_SMALL;
+
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* ws = (uint8_t*)workspace;
+  int32_t* hdr = (int32_t*)ws;
+  hipEvent_t* ev = (hipEvent_t*)d.prof_events;
+  const int G = d.num_q_heads / d.num_kv_heads;
+  const int e = fp8 ? 1 : 2;
+
+  if (ev && hipEventRecord(ev[0], s) != hipSuccess) return DORA_ERR_HIP;
+  if (validate) {
+    int32_t* err = hdr + 8;
+    if (launch_fill_i32(err, 0, 1, s) != hipSuccess) return DORA_ERR_HIP;
+    ValidateParams vp{block_table, seq_lens, version_ids, d.page_owner, d.num_seqs,
+                      d.page_size, d.block_table_stride, d.num_pages, err};
+    if (launch_validate(vp, s) != hipSuccess) return DORA_ERR_HIP;
+    int32_t host_err = 0;
+    if (hipMemcpyAsync(&host_err, err, 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+      return DORA_ERR_HIP;
+    if (host_err) return DORA_ERR_DEVICE_CHECK;
+  }
+
+  PlanParams pp;
+  pp.seq_lens = seq_lens;
+  pp.num_seqs = d.num_seqs;
+  pp.page_size = d.page_size;
+  pp.num_kv_heads = d.num_kv_heads;
+  pp.stride = d.block_table_stride;
+  pp.target_units = target_units_of(d);
+  pp.min_pages = kMinSplitPages;
+  pp.force_pages = (d.flags & DORA_FLAG_FORCE_SPLIT) ? d.split_pages : 0;
+  pp.hdr = hdr;
+  pp.seqinfo = (int2*)(ws + w.seqinfo_off);
+  pp.items = (int4*)(ws + w.items_off);
+  if (launch_plan(pp, s) != hipSuccess) return DORA_ERR_HIP;
+
+  if (ev && hipEventRecord(ev[1], s) != hipSuccess) return DORA_ERR_HIP;
+  DecodeParams dp;
+  dp.q = (const uint16_t*)q;
+  dp.k_pages = (const uint8_t*)k_pages;
+  dp.v_pages = (const uint8_t*)v_pages;
+  dp.k_scales = d.k_scales;
+  dp.v_scales = d.v_scales;
+  dp.block_table = block_table;
+  dp.seq_lens = seq_lens;
+  dp.out = (uint16_t*)out;
+  dp.hdr = hdr;
+  dp.items = pp.items;
+  dp.part_o = (float*)(ws + w.part_o_off);
+  dp.part_ml = (float2*)(ws + w.part_ml_off);
+  dp.num_q_heads = d.num_q_heads;
+  dp.num_kv_heads = d.num_kv_heads;
+  dp.group = G;
+  dp.stride = d.block_table_stride;
+  dp.page_bytes = (int64_t)d.num_kv_heads * d.page_size * d.head_dim * e;
+  const float scale = d.sm_scale > 0.f ? d.sm_scale : 1.0f / sqrtf((float)d.head_dim);
+  dp.scale_log2 = scale * 1.4426950408889634f;
+  const int64_t grid = w.max_items * d.num_kv_heads;
+  if (launch_split_decode(dp, d.head_dim, d.page_size, fp8, grid, s) != hipSuccess)
+    return DORA_ERR_HIP;
+
+  if (ev && hipEventRecord(ev[2], s) != hipSuccess) return DORA_ERR_HIP;
+  CombineParams cp{pp.seqinfo, dp.part_o, dp.part_ml, (uint16_t*)out, d.num_seqs,
+                   d.num_q_heads, d.num_kv_heads, G, d.head_dim};
+  if (launch_combine(cp, s) != hipSuccess) return DORA_ERR_HIP;
+  if (ev && hipEventRecord(ev[3], s) != hipSuccess) return DORA_ERR_HIP;
+  return DORA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// pack / unpack
+// ---------------------------------------------------------------------------
+
+static dora_status check_pack_desc(const dora_pack_desc* d) {
+  if (!d) return DORA_ERR_INVALID_ARG;
+  if (d->num_kv_heads < 1 || d->page_size < 1 || d->head_dim < 1 || d->num_pages < 1)
+    return DORA_ERR_INVALID_ARG;
+  if (d->kv_dtype != DORA_KV_BF16 && d->kv_dtype != DORA_KV_FP8_E4M3)
+    return DORA_ERR_UNSUPPORTED;
+  const int e = d->kv_dtype == DORA_KV_BF16 ? 2 : 1;
+  if (((int64_t)d->num_kv_heads * d->page_size * d->head_dim * e) % 16 != 0)
+    return DORA_ERR_UNSUPPORTED;
+  return DORA_OK;
+}
+
+size_t dora_kv_packed_bytes(const dora_pack_desc* desc, int64_t n_pages) {
+  if (check_pack_desc(desc) != DORA_OK || n_pages < 0) return 0;
+  const int e = desc->kv_dtype == DORA_KV_BF16 ? 2 : 1;
+  const int64_t pb = (int64_t)desc->num_kv_heads * desc->page_size * desc->head_dim * e;
+  size_t total = 256 + (size_t)(2 * n_pages * pb);
+  if (desc->kv_dtype == DORA_KV_FP8_E4M3) total += (size_t)(2 * n_pages * 4);
+  return total;
+}
+
+dora_status dora_kv_page_pack(const dora_pack_desc* desc, const void* k_pages,
+                              const void* v_pages, const float* k_scales,
+                              const float* v_scales, const int32_t* src_pages, int64_t n_pages,
+                              void* packed, size_t packed_bytes, dora_stream_t stream) {
+  dora_status st = check_pack_desc(desc);
+  if (st != DORA_OK) return st;
+  if (n_pages < 0 || !packed) return DORA_ERR_INVALID_ARG;
+  if (n_pages > 0 && (!k_pages || !v_pages || !src_pages)) return DORA_ERR_INVALID_ARG;
+  const bool fp8 = desc->kv_dtype == DORA_KV_FP8_E4M3;
+  if (fp8 && n_pages > 0 && (!k_scales || !v_scales)) return DORA_ERR_INVALID_ARG;
+  if (!aligned16(packed) || (n_pages > 0 && (!aligned16(k_pages) || !aligned16(v_pages))))
+    return DORA_ERR_INVALID_ARG;
+  if (packed_bytes < dora_kv_packed_bytes(desc, n_pages)) return DORA_ERR_WORKSPACE_TOO_SMALL;
+  PackParams p;
+  memset(&p, 0, sizeof p);
+  p.k_pages = (const uint8_t*)k_pages;
+  p.v_pages = (const uint8_t*)v_pages;
+  p.k_scales = k_scales;
+  p.v_scales = v_scales;
+  p.pages = src_pages;
+  p.n_pages = n_pages;
+  p.num_pages = desc->num_pages;
+  p.page_bytes = (int64_t)desc->num_kv_heads * desc->page_size * desc->head_dim * (fp8 ? 1 : 2);
+  p.packed = (uint8_t*)packed;
+  p.has_scales = fp8 ? 1 : 0;
+  make_pack_header(*desc, n_pages, &p.hdr);
+  return launch_pack(p, (hipStream_t)stream) == hipSuccess ? DORA_OK : DORA_ERR_HIP;
+}
+
+dora_status dora_kv_page_unpack(const dora_pack_desc* desc, int32_t src_version,
+                                const void* packed, size_t packed_bytes,
+                                const int32_t* dst_pages, int64_t n_pages, void* k_pages,
+                                void* v_pages, float* k_scales, float* v_scales,
+                                int32_t* dev_status, dora_stream_t stream) {
+  dora_status st = check_pack_desc(desc);
+  if (st != DORA_OK) return st;
+  if (src_version != desc->policy_version) return DORA_ERR_VERSION_MISMATCH;
+  if (n_pages < 0 || !packed) return DORA_ERR_INVALID_ARG;
+  if (n_pages > 0 && (!k_pages || !v_pages || !dst_pages)) return DORA_ERR_INVALID_ARG;
+  const bool fp8 = desc->kv_dtype == DORA_KV_FP8_E4M3;
+  if (fp8 && n_pages > 0 && (!k_scales || !v_scales)) return DORA_ERR_INVALID_ARG;
+  if (!aligned16(packed) || (n_pages > 0 && (!aligned16(k_pages) || !aligned16(v_pages))))
+    return DORA_ERR_INVALID_ARG;
+  if (packed_bytes < dora_kv_packed_bytes(desc, n_pages)) return DORA_ERR_WORKSPACE_TOO_SMALL;
+  PackParams p;
+  memset(&p, 0, sizeof p);
+  p.pages = dst_pages;
+  p.n_pages = n_pages;
+  p.num_pages = desc->num_pages;
+  p.page_bytes = (int64_t)desc->num_kv_heads * desc->page_size * desc->head_dim * (fp8 ? 1 : 2);
+  p.packed_in = (const uint8_t*)packed;
+  p.k_out = (uint8_t*)k_pages;
+  p.v_out = (uint8_t*)v_pages;
+  p.ks_out = k_scales;
+  p.vs_out = v_scales;
+  p.dev_status = dev_status;
+  p.has_scales = fp8 ? 1 : 0;
+  make_pack_header(*desc, n_pages, &p.hdr);
+  return launch_unpack(p, (hipStream_t)stream) == hipSuccess ? DORA_OK : DORA_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,184 @@
+"""CPU checks of the C ABI: the library loads, exports every symbol the header
+declares, and rejects bad arguments before any launch (no GPU is touched:
+every call here returns during host-side validation)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dora.h")
+
+
+@pytest.fixture(scope="module")
+def d():
+    from paper_2604_26256_amd import build as B
+    if not os.path.exists(B.LIB):
+        B.build()
+    from paper_2604_26256_amd import dora
+    return dora
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dora_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol(d):
+    names = _declared_functions()
+    assert len(names) >= 17, names
+    lib = d.library()
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings(d):
+    for code in range(9):
+        s = d.status_string(code)
+        assert s and s != "unknown status"
+    assert d.status_string(99) == "unknown status"
+
+
+def _desc(d, **kw):
+    base = dict(num_seqs=4, num_q_heads=8, num_kv_heads=2, head_dim=128, page_size=16,
+                block_table_stride=64, num_pages=1024)
+    base.update(kw)
+    return d.make_decode_desc(**base)
+
+
+def test_workspace_bytes(d):
+    ok = d.dora_decode_workspace_bytes(_desc(d))
+    assert ok > 0 and ok % 256 == 0
+    assert d.dora_decode_workspace_bytes(_desc(d, num_seqs=400)) > ok
+    assert d.dora_decode_workspace_bytes(_desc(d, num_q_heads=36, num_kv_heads=2)) == 0  # G=18
+    assert d.dora_decode_workspace_bytes(_desc(d, head_dim=96)) == 0
+    assert d.dora_decode_workspace_bytes(_desc(d, page_size=8)) == 0
+    assert d.dora_decode_workspace_bytes(_desc(d, num_q_heads=7)) == 0       # not a multiple
+    assert d.dora_decode_workspace_bytes(_desc(d, kv_dtype=5)) == 0
+    forced = _desc(d, flags=d.DORA_FLAG_FORCE_SPLIT, split_pages=1)
+    assert d.dora_decode_workspace_bytes(forced) >= 4 * 64 * 16
+
+
+FAKE = 0x10000  # aligned non-null stand-in; never dereferenced (calls fail validation)
+
+
+def _call(d, desc, q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, vid=FAKE, out=FAKE, ws=FAKE,
+          wsb=1 << 30):
+    P = ctypes.c_void_p
+    return d.library().dora_decode_attn(ctypes.byref(desc), P(q), P(k), P(v), P(bt), P(lens),
+                                        P(vid), P(out), P(ws), wsb, None)
+
+
+def test_decode_host_validation(d):
+    assert _call(d, _desc(d, num_q_heads=7)) == d.DORA_ERR_INVALID_ARG
+    assert _call(d, _desc(d, num_seqs=-1)) == d.DORA_ERR_INVALID_ARG
+    assert _call(d, _desc(d, block_table_stride=0)) == d.DORA_ERR_INVALID_ARG
+    assert _call(d, _desc(d, head_dim=96)) == d.DORA_ERR_UNSUPPORTED
+    assert _call(d, _desc(d, num_q_heads=34, num_kv_heads=2)) == d.DORA_ERR_UNSUPPORTED
+    assert _call(d, _desc(d, flags=0x80)) == d.DORA_ERR_INVALID_ARG
+    assert _call(d, _desc(d, flags=d.DORA_FLAG_FORCE_SPLIT)) == d.DORA_ERR_INVALID_ARG
+    assert _call(d, _desc(d, sm_scale=-1.0)) == d.DORA_ERR_INVALID_ARG
+    assert _call(d, _desc(d), q=0) == d.DORA_ERR_INVALID_ARG
+    assert _call(d, _desc(d), ws=0) == d.DORA_ERR_INVALID_ARG
+    assert _call(d, _desc(d), out=FAKE + 2) == d.DORA_ERR_INVALID_ARG          # misaligned
+    assert _call(d, _desc(d, kv_dtype=1)) == d.DORA_ERR_INVALID_ARG            # no fp8 scales
+    need = d.dora_decode_workspace_bytes(_desc(d))
+    assert _call(d, _desc(d), wsb=need - 1) == d.DORA_ERR_WORKSPACE_TOO_SMALL
+    assert _call(d, _desc(d, num_seqs=0)) == d.DORA_OK                         # nothing to do
+    assert d.library().dora_decode_attn(None, None, None, None, None, None, None, None, None, 0,
+                                        None) == d.DORA_ERR_INVALID_ARG
+
+
+def test_pack_host_validation_and_size(d):
+    lib = d.library()
+    for dt in (0, 1):
+        desc = d.make_pack_desc(kv_dtype=dt, page_size=16, num_kv_heads=8, head_dim=128,
+                                num_pages=100, policy_version=1)
+        for n in (0, 1, 37):
+            assert d.dora_kv_packed_bytes(desc, n) == oracle.packed_bytes(dt, 16, 8, 128, n)
+    desc = d.make_pack_desc(kv_dtype=0, page_size=16, num_kv_heads=8, head_dim=128,
+                            num_pages=100, policy_version=1)
+    P = ctypes.c_void_p
+    need = d.dora_kv_packed_bytes(desc, 3)
+    assert lib.dora_kv_page_pack(ctypes.byref(desc), P(FAKE), P(FAKE), None, None, P(FAKE), 3,
+                                 P(FAKE), need - 1, None) == d.DORA_ERR_WORKSPACE_TOO_SMALL
+    assert lib.dora_kv_page_pack(ctypes.byref(desc), P(FAKE), P(FAKE), None, None, None, 3,
+                                 P(FAKE), need, None) == d.DORA_ERR_INVALID_ARG
+    assert lib.dora_kv_page_unpack(ctypes.byref(desc), 2, P(FAKE), need, P(FAKE), 3, P(FAKE),
+                                   P(FAKE), None, None, None, None) == \
+        d.DORA_ERR_VERSION_MISMATCH
+    bad = d.make_pack_desc(kv_dtype=3, page_size=16, num_kv_heads=8, head_dim=128,
+                           num_pages=100, policy_version=1)
+    assert d.dora_kv_packed_bytes(bad, 1) == 0
+
+
+# ---------------------------------------------------------------------------
+# host page pool
+# ---------------------------------------------------------------------------
+
+def test_pool_alloc_free_and_ownership(d):
+    pool = d.Pool(64, 16, 3, seed=0)
+    a = pool.add_seq(0, 40)          # 3 pages
+    b = pool.add_seq(2, 16)          # 1 page
+    assert list(pool.seq_pages(a)) == [0, 1, 2] and list(pool.seq_pages(b)) == [3]
+    assert pool.stats(0) == (3, 60) and pool.stats(2) == (1, 60) and pool.stats(-1) == (4, 60)
+    own = pool.page_owner()
+    assert list(own[:4]) == [0, 0, 0, 2] and (own[4:] == -1).all()
+    pool.extend_seq(a, 49)           # 4 pages
+    assert pool.seq_info(a) == (49, 0, 4)
+    pool.free_seq(a)
+    assert pool.stats(0) == (0, 63)
+    assert (pool.page_owner() == np.array([-1, -1, -1, 2] + [-1] * 60)).all()
+    with pytest.raises(d.DoraError) as e:
+        pool.free_seq(a)
+    assert e.value.status == d.DORA_ERR_NOT_FOUND
+
+
+def test_pool_exhaustion_leaves_state_unchanged(d):
+    pool = d.Pool(10, 16, 1, seed=5)
+    a = pool.add_seq(0, 16 * 8)
+    before = (pool.stats(0), pool.page_owner().copy())
+    with pytest.raises(d.DoraError) as e:
+        pool.add_seq(0, 16 * 3)
+    assert e.value.status == d.DORA_ERR_POOL_EXHAUSTED
+    with pytest.raises(d.DoraError):
+        pool.extend_seq(a, 16 * 11)
+    assert pool.stats(0) == before[0] and (pool.page_owner() == before[1]).all()
+    assert pool.seq_info(a) == (128, 0, 8)
+
+
+def test_pool_seeded_scatter_and_block_table(d):
+    pool = d.Pool(4096, 16, 2, seed=1234)
+    ids = [pool.add_seq(i % 2, L) for i, L in enumerate([1, 100, 2000, 17])]
+    pages = np.concatenate([pool.seq_pages(i) for i in ids])
+    assert len(np.unique(pages)) == len(pages)
+    assert not np.array_equal(pages, np.arange(len(pages)))    # scattered
+    table, lens, vers = pool.block_table(ids)
+    assert table.shape == (4, 125) and list(lens) == [1, 100, 2000, 17]
+    assert list(vers) == [0, 1, 0, 1]
+    assert list(table[1, :7]) == list(pool.seq_pages(ids[1])) and not table[1, 7:].any()
+    with pytest.raises(d.DoraError):
+        pool.block_table(ids, stride=10)                        # sequence too long
+    again = d.Pool(4096, 16, 2, seed=1234)
+    ids2 = [again.add_seq(i % 2, L) for i, L in enumerate([1, 100, 2000, 17])]
+    assert np.array_equal(np.concatenate([again.seq_pages(i) for i in ids2]), pages)
+
+
+def test_pool_migration_rules(d):
+    src = d.Pool(256, 16, 3, seed=3)
+    dst = d.Pool(256, 16, 3, seed=4)
+    s = src.add_seq(1, 300)
+    with pytest.raises(d.DoraError) as e:
+        src.migrate_seq(s, dst, 2)                          # other version
+    assert e.value.status == d.DORA_ERR_VERSION_MISMATCH
+    same, sp, dp = src.migrate_seq(s, src, 1)               # locality: nothing moves
+    assert same == s and len(sp) == 0 and len(dp) == 0
+    nid, sp, dp = src.migrate_seq(s, dst, 1)
+    assert list(sp) == list(src.seq_pages(s)) and list(dp) == list(dst.seq_pages(nid))
+    assert dst.seq_info(nid) == (300, 1, 19) and dst.stats(1)[0] == 19
+    assert (dst.page_owner()[dp] == 1).all()

@@ -1,0 +1,197 @@
+"""GPU parity of dora_decode_attn (through the C ABI) against the fp64 oracle.
+
+Bar: max-abs error <= 2e-2 on bf16-KV outputs and <= 5e-2 on fp8-KV outputs;
+bitwise equality where the result is unique (length-1 sequences, page
+permutation, batch permutation, repeated runs).
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from gpu_util import TOL, gpu_batch, lib, max_abs_err, oracle_for, run_decode, sample_seqs
+
+pytestmark = pytest.mark.gpu
+
+
+def _w(name="t", B=8, Hq=8, Hkv=2, d=64, P=16, dt=0, pages=None, lens=None):
+    pages = pages or max(64, int(wl.pages_needed(np.asarray(lens), P).sum()) * 2 + 8)
+    return wl.Workload(name, B, Hq, Hkv, d, P, dt, pages, "uniform", lo=1, hi=1)
+
+
+RAGGED = [0, 1, 2, 15, 16, 17, 31, 32, 33, 100, 257, 1000, 4097]
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("P", [16, 32])
+@pytest.mark.parametrize("dt", [0, 1])
+@pytest.mark.parametrize("G", [1, 4, 7, 16])
+def test_shapes_ragged_lengths(d, P, dt, G):
+    print(f"[case] shapes d={d} P={P} dt={dt} G={G}", flush=True)
+    Hkv = 2
+    lens = np.array(RAGGED, np.int32)
+    w = _w(B=len(lens), Hq=G * Hkv, Hkv=Hkv, d=d, P=P, dt=dt, lens=lens)
+    b = gpu_batch(w, lengths=lens, seed_index=100 + d + P + dt + G)
+    out = run_decode(b)
+    ref = oracle_for(b)
+    err = max_abs_err(out, ref)
+    assert err <= TOL[dt], err
+    assert torch.all(out[0] == 0), "empty sequence must give zeros"
+
+
+def test_tiny_workload_full_parity():
+    w = wl.WORKLOADS[0]
+    print(f"[case] {w.name}", flush=True)
+    b = gpu_batch(w, seed_index=0)
+    out = run_decode(b)
+    err = max_abs_err(out, oracle_for(b))
+    assert err <= TOL[0], err
+
+
+@pytest.mark.parametrize("split", [1, 2, 3, 0, 100000])
+def test_split_invariance(split):
+    """Forced split sizes (pages) all agree with the oracle and with each other."""
+    print(f"[case] split={split}", flush=True)
+    lens = np.array([5, 700, 1300, 33, 2048, 16], np.int32)
+    w = _w(B=len(lens), Hq=16, Hkv=2, d=128, P=16, dt=0, lens=lens)
+    b = gpu_batch(w, lengths=lens, seed_index=7)
+    kw = {}
+    if split:
+        kw = dict(flags=lib().DORA_FLAG_FORCE_SPLIT, split_pages=split)
+    out = run_decode(b, **kw)
+    ref = oracle_for(b)
+    assert max_abs_err(out, ref) <= TOL[0]
+    base = run_decode(b)
+    diff = (out.float() - base.float()).abs().max().item()
+    assert diff <= TOL[0]
+
+
+def test_split_invariance_fp8_page32():
+    lens = np.array([2000, 64, 4500, 1], np.int32)
+    w = _w(B=len(lens), Hq=16, Hkv=2, d=128, P=32, dt=1, lens=lens)
+    b = gpu_batch(w, lengths=lens, seed_index=8)
+    ref = oracle_for(b)
+    for split in (1, 5, 1000):
+        out = run_decode(b, flags=lib().DORA_FLAG_FORCE_SPLIT, split_pages=split)
+        assert max_abs_err(out, ref) <= TOL[1]
+
+
+def test_deterministic_bitwise():
+    lens = np.array([3000, 17, 900, 4000, 1], np.int32)
+    w = _w(B=len(lens), Hq=28, Hkv=4, d=128, P=16, dt=0, lens=lens)
+    b = gpu_batch(w, lengths=lens, seed_index=9)
+    a = run_decode(b).clone()
+    for _ in range(3):
+        assert torch.equal(run_decode(b), a)
+
+
+def test_length_one_is_value_row_bitwise():
+    lens = np.ones(6, np.int32)
+    w = _w(B=6, Hq=8, Hkv=2, d=128, P=16, dt=0, lens=lens)
+    b = gpu_batch(w, lengths=lens, seed_index=10)
+    out = run_decode(b)
+    for s in range(6):
+        pg = int(b.block_table_h[s, 0])
+        for h in range(8):
+            v = b.v_pages[pg, h // 4, :, 0]          # token slot 0, all head dims
+            assert torch.equal(out[s, h], v)
+
+
+def test_physical_page_permutation_bitwise():
+    lens = np.array([300, 1, 77, 1024], np.int32)
+    w = _w(B=4, Hq=8, Hkv=2, d=128, P=16, dt=0, lens=lens)
+    b = gpu_batch(w, lengths=lens, seed_index=11)
+    ref = run_decode(b).clone()
+    perm = torch.randperm(w.num_pages, generator=torch.Generator().manual_seed(3)).cuda()
+    k2 = torch.empty_like(b.k_pages)
+    v2 = torch.empty_like(b.v_pages)
+    k2[perm] = b.k_pages
+    v2[perm] = b.v_pages
+    bt2 = perm[b.block_table.long()].to(torch.int32)
+    b.k_pages, b.v_pages, b.block_table = k2, v2, bt2.contiguous()
+    assert torch.equal(run_decode(b), ref)
+
+
+def test_batch_permutation_bitwise():
+    lens = np.array([300, 1, 77, 1024, 5000, 0], np.int32)
+    w = _w(B=6, Hq=8, Hkv=2, d=128, P=16, dt=0, lens=lens)
+    b = gpu_batch(w, lengths=lens, seed_index=12)
+    ref = run_decode(b).clone()
+    perm = torch.tensor([3, 5, 0, 4, 1, 2])
+    b.q = b.q[perm.cuda()].contiguous()
+    b.block_table = b.block_table[perm.cuda()].contiguous()
+    b.seq_lens = b.seq_lens[perm.cuda()].contiguous()
+    b.version_ids = b.version_ids[perm.cuda()].contiguous()
+    assert torch.equal(run_decode(b), ref[perm.cuda()])
+
+
+def test_workspace_contents_ignored():
+    lens = np.array([800, 2000, 3], np.int32)
+    w = _w(B=3, Hq=8, Hkv=2, d=128, P=16, dt=0, lens=lens)
+    b = gpu_batch(w, lengths=lens, seed_index=13)
+    d = lib()
+    ref = run_decode(b, flags=d.DORA_FLAG_FORCE_SPLIT, split_pages=4).clone()
+    desc = d.make_decode_desc(num_seqs=3, num_q_heads=8, num_kv_heads=2, head_dim=128,
+                              page_size=16, block_table_stride=b.stride,
+                              num_pages=w.num_pages, flags=d.DORA_FLAG_FORCE_SPLIT,
+                              split_pages=4)
+    ws = torch.full((d.dora_decode_workspace_bytes(desc) // 4,), float("nan"),
+                    device="cuda").view(torch.uint8)
+    out = torch.full_like(b.q, float("nan"))
+    run_decode(b, out=out, flags=d.DORA_FLAG_FORCE_SPLIT, split_pages=4, workspace=ws)
+    assert torch.equal(out, ref)
+
+
+def test_validate_flag_accepts_good_and_rejects_bad_pages():
+    w = wl.WORKLOADS[3].scaled(48, num_pages=8192)   # three versions in one pool
+    b = gpu_batch(w, seed_index=3, lengths=np.random.default_rng(1).integers(1, 1500, 48)
+                  .astype(np.int32))
+    d = lib()
+    run_decode(b, flags=d.DORA_FLAG_VALIDATE, page_owner=b.page_owner)
+    # a page of another version in sequence 0's table
+    other = int(np.nonzero(b.versions_h != b.versions_h[0])[0][0])
+    bt = b.block_table.clone()
+    bt[0, 0] = b.block_table[other, 0]
+    b2 = b
+    b2.block_table = bt
+    with pytest.raises(d.DoraError) as e:
+        run_decode(b2, flags=d.DORA_FLAG_VALIDATE, page_owner=b.page_owner)
+    assert e.value.status == d.DORA_ERR_DEVICE_CHECK
+    bt = bt.clone()
+    bt[0, 0] = w.num_pages + 5
+    b2.block_table = bt
+    with pytest.raises(d.DoraError) as e:
+        run_decode(b2, flags=d.DORA_FLAG_VALIDATE)
+    assert e.value.status == d.DORA_ERR_DEVICE_CHECK
+
+
+def test_empty_batch_is_a_no_op():
+    d = lib()
+    q = torch.empty((0, 8, 64), dtype=torch.bfloat16, device="cuda")
+    kp = torch.zeros((4, 2, 8, 16, 8), dtype=torch.bfloat16, device="cuda")
+    vp = torch.zeros((4, 2, 64, 16), dtype=torch.bfloat16, device="cuda")
+    bt = torch.zeros((0, 1), dtype=torch.int32, device="cuda")
+    z = torch.zeros(0, dtype=torch.int32, device="cuda")
+    d.dora_decode_attn(q, kp, vp, bt, z, z, q.clone(), num_kv_heads=2, page_size=16)
+
+
+# ---------------------------------------------------------------------------
+# the five workloads at full size, in the launch configuration the benchmark
+# times; the oracle checks a sample of sequences (longest, shortest, median,
+# random) and every output is checked for finiteness.
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4])
+def test_full_size_workloads_sampled(idx):
+    w = wl.WORKLOADS[idx]
+    print(f"[case] full-size {w.name}", flush=True)
+    b = gpu_batch(w, seed_index=idx)
+    out = run_decode(b)
+    assert torch.isfinite(out.float()).all()
+    seqs = sample_seqs(b.lengths, 3, seed=idx)
+    ref = oracle_for(b, seqs)
+    err = max_abs_err(out, ref, seqs)
+    print(f"[case] {w.name}: sampled {len(seqs)} seqs, max-abs err {err:.3e}", flush=True)
+    assert err <= TOL[w.kv_dtype], err
+    del b
+    torch.cuda.empty_cache()

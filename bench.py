@@ -1,0 +1,371 @@
+"""Benchmark of the decode-attention hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--only-main]
+                    [--no-cpu-baseline] [--no-flush] [--gpus 1]
+
+One step = one dora_decode_attn call (stream-K decode kernel + combine) over
+one synthetic long-tailed decode batch whose inputs are already resident in
+HBM.  Caches (256 MB Infinity Cache, 8 x 4 MB L2) are evicted by a 1 GiB read
+before every step, outside the timed events.  The main line is the
+7B-class rollout batch (64 sequences, lognormal lengths with median 2048);
+the other workloads and the pack/unpack copy are reported under "workloads".
+
+Prints one JSON line.  value = decode tokens/s = sequences / step time (every
+sequence advances one token per step).  roofline: the decode kernel's
+algorithmic bytes (K and V of valid tokens, page scales, Q, output, block
+table and lengths) over its average duration, measured with HIP events that
+the library records around each kernel on the launch stream.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as wl  # noqa: E402
+
+METRIC = "decode-attn tokens/s and HBM GB/s (% of peak) on long-tail length mixes"
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+MAIN_WORKLOAD = "rollout7b"
+PROFILE_PMC = os.path.join(ROOT, "profiles", "split_decode_rollout7b_pmc.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2604_26256_amd", "csrc", f)
+                  for f in ("decode.hip", "dora_internal.h", "api.cpp")]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=MAIN_WORKLOAD, choices=[w.name for w in wl.WORKLOADS])
+    ap.add_argument("--only-main", action="store_true", help="skip the other workloads")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-flush", action="store_true")
+    ap.add_argument("--flush-mode", choices=["read", "write"], default="read",
+                    help="evict caches by reading (clean lines) or writing 1 GiB")
+    ap.add_argument("--num-waves", type=int, default=0,
+                    help="decode wavefronts (0 = one per resident slot)")
+    return ap.parse_args()
+
+
+def make_events(torch, n):
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    for e in evs:
+        e.record()
+    torch.cuda.synchronize()
+    return evs
+
+
+def time_decode(torch, dora, b, steps, warmup, flush, num_waves=0):
+    """Returns dict of per-step and per-kernel timings (ms)."""
+    w = b.w
+    out = torch.empty_like(b.q)
+    kw = dict(num_kv_heads=w.num_kv_heads, page_size=w.page_size, kv_dtype=w.kv_dtype,
+              k_scales=b.k_scales, v_scales=b.v_scales, num_waves=num_waves)
+
+    def call(prof=None):
+        dora.dora_decode_attn(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens,
+                              b.version_ids, out, prof_events=prof, **kw)
+
+    for _ in range(warmup):
+        flush()
+        call()
+    torch.cuda.synchronize()
+    # (a) whole steps: events bracket the call only; the flush sits outside them
+    starts = make_events(torch, steps)
+    ends = make_events(torch, steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        flush()
+        starts[i].record()
+        call()
+        ends[i].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
+    # (b) per kernel: the library records events before the decode kernel,
+    # between it and the combine kernel, and after the combine kernel
+    ev = make_events(torch, 3)
+    handles = [e.cuda_event for e in ev]
+    split, comb = [], []
+    for i in range(steps):
+        flush()
+        call(prof=handles)
+        torch.cuda.synchronize()
+        split.append(ev[0].elapsed_time(ev[1]))
+        comb.append(ev[1].elapsed_time(ev[2]))
+    return {"step_ms": step_ms, "wall_s": wall, "split_ms": np.array(split),
+            "combine_ms": np.array(comb), "out": out}
+
+
+def decode_record(w, lengths, t):
+    ab = wl.algorithmic_bytes(w, lengths)
+    st = wl.skew_stats(lengths)
+    ms = float(np.mean(t["step_ms"]))
+    split_ms = float(np.mean(t["split_ms"]))
+    return {
+        "ms_per_step": ms,
+        "ms_p10_p50_p90": [float(np.percentile(t["step_ms"], q)) for q in (10, 50, 90)],
+        "decode_tokens_per_s": w.num_seqs / (ms * 1e-3),
+        "context_tokens_per_s": st["sum"] / (ms * 1e-3),
+        "hbm_gbps": ab["total"] / (ms * 1e-3) / 1e9,
+        "hbm_frac_of_peak": ab["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "split_kernel_ms": split_ms,
+        "split_kernel_gbps": ab["total"] / (split_ms * 1e-3) / 1e9,
+        "combine_ms": float(np.mean(t["combine_ms"])),
+        "algorithmic_bytes": ab,
+        "lengths": {k: (round(v, 3) if isinstance(v, float) else v) for k, v in st.items()},
+    }
+
+
+def time_pack(torch, dora, b, steps, flush):
+    """Pack + unpack of the 32-sequence same-version migration set."""
+    w = b.w
+    rng = np.random.default_rng(5)
+    cand = np.nonzero(b.versions_h == 0)[0]
+    seqs = np.sort(rng.choice(cand, size=min(w.pack_seqs or 32, len(cand)), replace=False))
+    n = wl.pages_needed(b.lengths, w.page_size)
+    src = np.concatenate([b.block_table_h[s, :n[s]] for s in seqs]).astype(np.int32)
+    npg = len(src)
+    free = np.setdiff1d(np.arange(w.num_pages), b.used_pages)[:npg].astype(np.int32)
+    src_t = torch.from_numpy(src).cuda()
+    dst_t = torch.from_numpy(free).cuda()
+    desc = dora.make_pack_desc(kv_dtype=w.kv_dtype, page_size=w.page_size,
+                               num_kv_heads=w.num_kv_heads, head_dim=w.head_dim,
+                               num_pages=w.num_pages, policy_version=0)
+    packed = torch.empty(dora.dora_kv_packed_bytes(desc, npg), dtype=torch.uint8, device="cuda")
+    geo = dict(num_kv_heads=w.num_kv_heads, page_size=w.page_size, head_dim=w.head_dim,
+               kv_dtype=w.kv_dtype)
+    pk, up = [], []
+    for i in range(steps + 2):
+        flush()
+        s0, s1, s2 = make_events(torch, 3)
+        s0.record()
+        dora.dora_kv_page_pack(b.k_pages, b.v_pages, src_t, packed, policy_version=0,
+                               n_seqs=len(seqs), **geo)
+        s1.record()
+        flush()
+        torch.cuda.synchronize()
+        s1b = make_events(torch, 1)[0]
+        s1b.record()
+        dora.dora_kv_page_unpack(packed, dst_t, b.k_pages, b.v_pages, src_version=0,
+                                 policy_version=0, **geo)
+        s2.record()
+        torch.cuda.synchronize()
+        if i >= 2:
+            pk.append(s0.elapsed_time(s1))
+            up.append(s1b.elapsed_time(s2))
+    moved = 2 * npg * w.page_bytes          # K and V pages, one way
+    return {"seqs": int(len(seqs)), "pages": int(npg), "bytes_one_way": int(moved),
+            "pack_ms": float(np.mean(pk)), "unpack_ms": float(np.mean(up)),
+            "pack_gbps_rw": 2 * moved / (np.mean(pk) * 1e-3) / 1e9,
+            "unpack_gbps_rw": 2 * moved / (np.mean(up) * 1e-3) / 1e9}
+
+
+def copy_bandwidth(torch, nbytes=2 << 30):
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1)
+    c = torch.empty_like(a)
+    for _ in range(3):
+        c.copy_(a)
+    s, e = make_events(torch, 2)
+    s.record()
+    for _ in range(10):
+        c.copy_(a)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / 10
+    del a, c
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def cpu_baseline(b, budget_s=20.0):
+    """The fp64 oracle on the host cores over the same batch (or a prefix of
+    its sequences that fits the time budget), scaled to decode tokens/s."""
+    import oracle
+
+    cores = min(16, len(os.sched_getaffinity(0)))
+    order = list(range(b.w.num_seqs))
+    # calibrate on one sequence, then take as many sequences as the budget allows
+    probe = wl.subset_for_oracle(b, order[:1])
+    t0 = time.perf_counter()
+    oracle.decode(probe["q"], probe["k_pages"], probe["v_pages"], probe["block_table"],
+                  probe["seq_lens"], num_kv_heads=b.w.num_kv_heads, page_size=b.w.page_size,
+                  kv_dtype=b.w.kv_dtype, k_scales=probe["k_scales"],
+                  v_scales=probe["v_scales"], num_pages=probe["num_pages"], nthreads=cores)
+    per_tok = (time.perf_counter() - t0) / max(1, int(b.lengths[0]))
+    take, acc = [], 0.0
+    for s in order:
+        take.append(s)
+        acc += per_tok * int(b.lengths[s]) / cores
+        if acc >= budget_s:
+            break
+    sub = wl.subset_for_oracle(b, take)
+    t0 = time.perf_counter()
+    oracle.decode(sub["q"], sub["k_pages"], sub["v_pages"], sub["block_table"],
+                  sub["seq_lens"], num_kv_heads=b.w.num_kv_heads, page_size=b.w.page_size,
+                  kv_dtype=b.w.kv_dtype, k_scales=sub["k_scales"], v_scales=sub["v_scales"],
+                  num_pages=sub["num_pages"], nthreads=cores)
+    dt = time.perf_counter() - t0
+    ctx = int(b.lengths[take].sum())
+    # one decode step of the whole batch costs sum(L) context tokens of work
+    step_s = dt * float(b.lengths.sum()) / ctx
+    return {"value": b.w.num_seqs / step_s, "unit": "tokens/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"{len(take)} of {b.w.num_seqs} sequences ({ctx} context tokens, "
+                      f"{dt:.2f} s), scaled by total/sampled context tokens",
+            "cpu_model": _cpu_model()}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def load_pmc_traffic(w, lengths):
+    """HBM traffic of the split kernel from the committed rocprofv3 counter
+    summary, or None if absent or taken on a different kernel source."""
+    try:
+        with open(PROFILE_PMC) as f:
+            pmc = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if pmc.get("kernel_source_hash") != kernel_source_hash() or pmc.get("workload") != w.name:
+        return None
+    return pmc.get("traffic_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the decode path shards by sequence with no exchange; see DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2604_26256_amd import dora
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    flush_buf = None if args.no_flush else torch.ones(1 << 28, dtype=torch.float32,
+                                                     device="cuda")
+    flush_out = torch.empty((), dtype=torch.float32, device="cuda")
+    if flush_buf is None:
+        flush = lambda: None  # noqa: E731
+    elif args.flush_mode == "read":
+        # a 1 GiB read leaves only clean lines behind, so no write-back lands
+        # inside the next timed step
+        flush = lambda: torch.sum(flush_buf, dim=0, out=flush_out)  # noqa: E731
+    else:
+        flush = lambda: flush_buf.fill_(1.0)  # noqa: E731
+
+    names = [args.workload] + ([] if args.only_main else
+                               [w.name for w in wl.WORKLOADS if w.name != args.workload])
+    results, main_rec, main_t, main_batch = {}, None, None, None
+    cpu = None
+    for name in names:
+        w = wl.BY_NAME[name]
+        idx = wl.WORKLOADS.index(w)
+        log(f"workload {name}: generating")
+        b = wl.make_batch(w, device="cuda", seed_index=idx)
+        torch.cuda.synchronize()
+        steps = args.steps if name == args.workload else max(5, args.steps // 3)
+        log(f"workload {name}: timing {steps} steps")
+        t = time_decode(torch, dora, b, steps, args.warmup if name == args.workload else 2,
+                        flush, args.num_waves)
+        rec = decode_record(w, b.lengths, t)
+        rec["kv_dtype"] = "bf16" if w.kv_dtype == 0 else "fp8_e4m3"
+        if w.pack_seqs:
+            log(f"workload {name}: pack/unpack")
+            rec["pack_unpack"] = time_pack(torch, dora, b, max(5, steps // 2), flush)
+        results[name] = rec
+        log(f"workload {name}: {rec['ms_per_step']:.4f} ms/step, "
+            f"{rec['hbm_gbps']:.0f} GB/s, split kernel {rec['split_kernel_gbps']:.0f} GB/s")
+        if name == args.workload:
+            main_rec, main_t, main_batch = rec, t, b
+            main_rec["steps_wall_s"] = t["wall_s"]
+            if not args.no_cpu_baseline:
+                log("cpu baseline (oracle)")
+                cpu = cpu_baseline(b)
+        else:
+            del b
+        torch.cuda.empty_cache()
+
+    copy_gbps = copy_bandwidth(torch)
+    w = main_batch.w
+    ab = main_rec["algorithmic_bytes"]["total"]
+    split_s = main_rec["split_kernel_ms"] * 1e-3
+    traffic = load_pmc_traffic(w, main_batch.lengths)
+    line = {
+        "metric": METRIC,
+        "value": main_rec["decode_tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_rec["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.kv_dtype == 0 else "fp8_e4m3 KV, bf16 Q",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "num_seqs": w.num_seqs, "num_q_heads": w.num_q_heads,
+            "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "page_size": w.page_size,
+            "kv_dtype": main_rec["kv_dtype"], "pool_pages": w.num_pages,
+            "lengths": f"{w.length_law}(median {w.median}, sigma {w.sigma}) clipped "
+                       f"[{w.lo}, {w.hi}]" if w.length_law == "lognormal"
+                       else f"uniform [{w.lo}, {w.hi}]",
+            "parallelism": "single GPU",
+        },
+        "hbm_gbps": main_rec["hbm_gbps"],
+        "hbm_frac_of_peak": main_rec["hbm_frac_of_peak"],
+        "context_tokens_per_s": main_rec["context_tokens_per_s"],
+        "copy_gbps_measured": copy_gbps,
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "decode_kernel",
+            "achieved": ab / split_s / 1e9,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": ab / split_s / 1e9 / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": ab,
+            "avg_launch_ms": main_rec["split_kernel_ms"],
+        },
+        "cpu_baseline": cpu,
+        "flush_between_steps": None if args.no_flush else args.flush_mode,
+        "workloads": results,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -92,8 +92,6 @@ typedef enum {
 #define DORA_FLAG_VALIDATE    0x1u  /* range- and ownership-check every page id read;
                                        synchronises the stream and returns
                                        DORA_ERR_DEVICE_CHECK on bad device data */
-#define DORA_FLAG_FORCE_SPLIT 0x2u  /* use split_pages pages per KV split instead of
-                                       the balanced choice (split-invariance tests) */
 
 /* Geometry and options of one decode-attention call.  Supported builds:
  * head_dim in {64, 128}; page_size in {16, 32}; group size num_q_heads /
@@ -113,22 +111,25 @@ typedef struct {
   const int16_t* page_owner;   /* device [num_pages] owning version, or NULL; read
                                   only under DORA_FLAG_VALIDATE */
   uint32_t flags;              /* DORA_FLAG_* */
-  int32_t split_pages;         /* pages per split under DORA_FLAG_FORCE_SPLIT */
-  int32_t target_units;        /* target number of (sequence, KV head, split)
-                                  work units; 0 = library default */
-  void**  prof_events;         /* NULL, or 4 caller-created hipEvent_t recorded on
-                                  `stream` before the plan kernel, before the
-                                  split kernel, before the combine kernel and
-                                  after it (per-kernel timing) */
+  int32_t num_waves;           /* decode wavefronts to launch; 0 = one per
+                                  resident wavefront slot of the current device
+                                  (compute units x occupancy) */
+  int32_t min_range_pages;     /* smallest work range per wavefront, in
+                                  (page, KV head) units; 0 = library default */
+  void**  prof_events;         /* NULL, or 3 caller-created hipEvent_t recorded on
+                                  `stream` before the decode kernel, between it
+                                  and the combine kernel, and after the combine
+                                  kernel (per-kernel timing) */
 } dora_decode_desc;
 
 /* Human-readable name of a status code (static storage). */
 const char* dora_status_string(dora_status s);
 
-/* Bytes of device workspace dora_decode_attn needs for this geometry (an upper
- * bound over every seq_lens the call may see).  Returns 0 for an invalid or
- * unsupported descriptor.  The workspace holds the split plan and the per-split
- * partial results (unnormalised output, running max and sum in fp32). */
+/* Bytes of device workspace dora_decode_attn needs for this geometry on the
+ * current device (valid for every seq_lens the call may see).  Returns 0 for an
+ * invalid or unsupported descriptor.  The workspace holds the batch's page
+ * prefix and two partial results per decode wavefront (unnormalised output,
+ * running max and sum in fp32). */
 size_t dora_decode_workspace_bytes(const dora_decode_desc* desc);
 
 /* Decode-step attention over the paged, multi-version KV pool (the operation
@@ -145,9 +146,11 @@ size_t dora_decode_workspace_bytes(const dora_decode_desc* desc);
  *   out          device bf16 [B][Hq][d], written for every (b, h)
  *   workspace    device, >= dora_decode_workspace_bytes(desc) bytes, 16-byte
  *                aligned; contents on entry are ignored
- * Launches a plan kernel, the split-KV decode kernel and a log-sum-exp combine
- * kernel on `stream`.  Results do not depend on the split choice beyond fp32
- * rounding, and repeated calls on the same inputs are bitwise identical. */
+ * Launches the decode kernel and a log-sum-exp combine kernel on `stream` (per
+ * 8192 sequences).  Every decode wavefront takes an equal share of the batch's
+ * (page, KV head) work, whatever the length mix.  Results do not depend on the
+ * number of wavefronts beyond fp32 rounding, and repeated calls on the same
+ * inputs and device are bitwise identical. */
 dora_status dora_decode_attn(const dora_decode_desc* desc,
                              const void* q, const void* k_pages, const void* v_pages,
                              const int32_t* block_table, const int32_t* seq_lens,

@@ -22,7 +22,11 @@ bool geometry_supported(const dora_decode_desc& d) {
   if (d.page_size != 16 && d.page_size != 32) return false;
   if (d.kv_dtype != DORA_KV_BF16 && d.kv_dtype != DORA_KV_FP8_E4M3) return false;
   const int G = d.num_q_heads / d.num_kv_heads;
-  return G >= 1 && G <= 16;
+  // the decode kernel's page-head descriptor holds g in 7 bits and j in 19, and
+  // its page prefix and page-head indices are 32-bit
+  const int64_t seqs = d.num_seqs < kMaxSeqsPerLaunch ? d.num_seqs : kMaxSeqsPerLaunch;
+  return G >= 1 && G <= 16 && d.num_kv_heads <= 127 && d.block_table_stride < (1 << 19) &&
+         seqs * d.block_table_stride * d.num_kv_heads < ((int64_t)1 << 31);
 }
 
 // Host-checkable validity of a descriptor (pointers are checked separately).
@@ -31,46 +35,48 @@ dora_status check_desc(const dora_decode_desc* d) {
   if (d->num_seqs < 0 || d->num_kv_heads < 1 || d->num_q_heads < 1 ||
       d->num_q_heads % d->num_kv_heads != 0 || d->block_table_stride < 1 ||
       d->num_pages < 1 || d->head_dim < 1 || d->page_size < 1 || !(d->sm_scale >= 0.f) ||
-      d->target_units < 0 || (d->flags & ~(DORA_FLAG_VALIDATE | DORA_FLAG_FORCE_SPLIT)) != 0)
+      d->num_waves < 0 || d->min_range_pages < 0 || (d->flags & ~DORA_FLAG_VALIDATE) != 0)
     return DORA_ERR_INVALID_ARG;
-  if ((d->flags & DORA_FLAG_FORCE_SPLIT) && d->split_pages < 1) return DORA_ERR_INVALID_ARG;
   if (!geometry_supported(*d)) return DORA_ERR_UNSUPPORTED;
   return DORA_OK;
 }
 
-int target_units_of(const dora_decode_desc& d) {
-  return d.target_units > 0 ? d.target_units : kDefaultTargetUnits;
+int min_range_of(const dora_decode_desc& d) {
+  return d.min_range_pages > 0 ? d.min_range_pages : kMinRangePages;
 }
 
 }  // namespace
 
 namespace dora {
 
-bool ws_layout(const dora_decode_desc& d, WsLayout* out) {
-  const int64_t B = d.num_seqs;
-  const int64_t Hkv = d.num_kv_heads;
-  const int64_t G = d.num_q_heads / d.num_kv_heads;
-  int64_t items;
-  if (d.flags & DORA_FLAG_FORCE_SPLIT) {
-    // every sequence holds at most block_table_stride pages
-    items = B * ((d.block_table_stride + d.split_pages - 1) / d.split_pages);
-  } else {
-    // sum_b max(1, ceil(n_b / C)) <= total / C + B <= target / Hkv + B
-    const int64_t tu = target_units_of(d);
-    items = (tu + Hkv - 1) / Hkv + B;
+int64_t decode_waves(const dora_decode_desc& d) {
+  if (d.num_waves > 0) return d.num_waves;
+  int dev = 0, cus = 0, per_cu = 0;
+  const int seqs = d.num_seqs < kMaxSeqsPerLaunch ? d.num_seqs : kMaxSeqsPerLaunch;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      decode_waves_per_cu(d.head_dim, d.page_size, d.kv_dtype == DORA_KV_FP8_E4M3, seqs,
+                          &per_cu) != hipSuccess ||
+      cus <= 0 || per_cu <= 0) {
+    (void)hipGetLastError();  // no device here: size for a 256-CU part at 8 waves per CU
+    cus = 256;
+    per_cu = 8;
   }
-  if (items < 1) items = 1;
+  return (int64_t)cus * per_cu * kWaveFactor;
+}
+
+bool ws_layout(const dora_decode_desc& d, int64_t waves, WsLayout* out) {
+  const int64_t B = d.num_seqs < kMaxSeqsPerLaunch ? d.num_seqs : kMaxSeqsPerLaunch;
+  const int64_t G = d.num_q_heads / d.num_kv_heads;
   WsLayout w;
-  w.max_items = items;
+  w.waves = waves;
   size_t off = kWsHeaderBytes;
-  w.seqinfo_off = off;
-  off = align_up(off + (size_t)B * 8);
-  w.items_off = off;
-  off = align_up(off + (size_t)items * 16);
+  w.prefix_off = off;
+  off = align_up(off + (size_t)(B + 1) * 4);
   w.part_o_off = off;
-  off = align_up(off + (size_t)items * Hkv * G * d.head_dim * 4);
+  off = align_up(off + (size_t)(2 * waves) * G * d.head_dim * 4);
   w.part_ml_off = off;
-  off = align_up(off + (size_t)items * Hkv * G * 8);
+  off = align_up(off + (size_t)(2 * waves) * G * 8);
   w.total = off;
   *out = w;
   return true;
@@ -98,7 +104,7 @@ const char* dora_status_string(dora_status s) {
 size_t dora_decode_workspace_bytes(const dora_decode_desc* desc) {
   if (check_desc(desc) != DORA_OK) return 0;
   WsLayout w;
-  if (!ws_layout(*desc, &w)) return 0;
+  if (!ws_layout(*desc, decode_waves(*desc), &w)) return 0;
   return w.total;
 }
 
@@ -120,19 +126,17 @@ dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const 
       !aligned16(workspace))
     return DORA_ERR_INVALID_ARG;
   WsLayout w;
-  ws_layout(d, &w);
+  ws_layout(d, decode_waves(d), &w);
   if (workspace_bytes < w.total) return DORA_ERR_WORKSPACE_TOO_SMALL;
 
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace;
-  int32_t* hdr = (int32_t*)ws;
   hipEvent_t* ev = (hipEvent_t*)d.prof_events;
   const int G = d.num_q_heads / d.num_kv_heads;
   const int e = fp8 ? 1 : 2;
 
-  if (ev && hipEventRecord(ev[0], s) != hipSuccess) return DORA_ERR_HIP;
   if (validate) {
-    int32_t* err = hdr + 8;
+    int32_t* err = (int32_t*)ws;
     if (launch_fill_i32(err, 0, 1, s) != hipSuccess) return DORA_ERR_HIP;
     ValidateParams vp{block_table, seq_lens, version_ids, d.page_owner, d.num_seqs,
                       d.page_size, d.block_table_stride, d.num_pages, err};
@@ -144,50 +148,39 @@ dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const 
     if (host_err) return DORA_ERR_DEVICE_CHECK;
   }
 
-  PlanParams pp;
-  pp.seq_lens = seq_lens;
-  pp.num_seqs = d.num_seqs;
-  pp.page_size = d.page_size;
-  pp.num_kv_heads = d.num_kv_heads;
-  pp.stride = d.block_table_stride;
-  pp.target_units = target_units_of(d);
-  pp.min_pages = kMinSplitPages;
-  pp.force_pages = (d.flags & DORA_FLAG_FORCE_SPLIT) ? d.split_pages : 0;
-  pp.hdr = hdr;
-  pp.seqinfo = (int2*)(ws + w.seqinfo_off);
-  pp.items = (int4*)(ws + w.items_off);
-  if (launch_plan(pp, s) != hipSuccess) return DORA_ERR_HIP;
-
-  if (ev && hipEventRecord(ev[1], s) != hipSuccess) return DORA_ERR_HIP;
-  DecodeParams dp;
-  dp.q = (const uint16_t*)q;
-  dp.k_pages = (const uint8_t*)k_pages;
-  dp.v_pages = (const uint8_t*)v_pages;
-  dp.k_scales = d.k_scales;
-  dp.v_scales = d.v_scales;
-  dp.block_table = block_table;
-  dp.seq_lens = seq_lens;
-  dp.out = (uint16_t*)out;
-  dp.hdr = hdr;
-  dp.items = pp.items;
-  dp.part_o = (float*)(ws + w.part_o_off);
-  dp.part_ml = (float2*)(ws + w.part_ml_off);
-  dp.num_q_heads = d.num_q_heads;
-  dp.num_kv_heads = d.num_kv_heads;
-  dp.group = G;
-  dp.stride = d.block_table_stride;
-  dp.page_bytes = (int64_t)d.num_kv_heads * d.page_size * d.head_dim * e;
   const float scale = d.sm_scale > 0.f ? d.sm_scale : 1.0f / sqrtf((float)d.head_dim);
-  dp.scale_log2 = scale * 1.4426950408889634f;
-  const int64_t grid = w.max_items * d.num_kv_heads;
-  if (launch_split_decode(dp, d.head_dim, d.page_size, fp8, grid, s) != hipSuccess)
-    return DORA_ERR_HIP;
-
+  const int64_t qrow = (int64_t)d.num_q_heads * d.head_dim;  // elements per sequence
+  if (ev && hipEventRecord(ev[0], s) != hipSuccess) return DORA_ERR_HIP;
+  for (int c0 = 0; c0 < d.num_seqs; c0 += kMaxSeqsPerLaunch) {
+    const int nb = d.num_seqs - c0 < kMaxSeqsPerLaunch ? d.num_seqs - c0 : kMaxSeqsPerLaunch;
+    DecodeParams dp;
+    dp.q = (const uint16_t*)q + c0 * qrow;
+    dp.k_pages = (const uint8_t*)k_pages;
+    dp.v_pages = (const uint8_t*)v_pages;
+    dp.k_scales = d.k_scales;
+    dp.v_scales = d.v_scales;
+    dp.block_table = block_table + (int64_t)c0 * d.block_table_stride;
+    dp.seq_lens = seq_lens + c0;
+    dp.out = (uint16_t*)out + c0 * qrow;
+    dp.prefix = (int32_t*)(ws + w.prefix_off);
+    dp.part_o = (float*)(ws + w.part_o_off);
+    dp.part_ml = (float2*)(ws + w.part_ml_off);
+    dp.num_seqs = nb;
+    dp.num_q_heads = d.num_q_heads;
+    dp.num_kv_heads = d.num_kv_heads;
+    dp.group = G;
+    dp.stride = d.block_table_stride;
+    dp.min_range = min_range_of(d);
+    dp.page_bytes = (int64_t)d.num_kv_heads * d.page_size * d.head_dim * e;
+    dp.scale_log2 = scale * 1.4426950408889634f;
+    if (launch_decode(dp, d.head_dim, d.page_size, fp8, w.waves, s) != hipSuccess)
+      return DORA_ERR_HIP;
+    if (ev && c0 == 0 && hipEventRecord(ev[1], s) != hipSuccess) return DORA_ERR_HIP;
+    CombineParams cp{dp.prefix, dp.part_o, dp.part_ml, dp.out, nb, d.num_q_heads,
+                     d.num_kv_heads, G, d.head_dim, dp.min_range, w.waves};
+    if (launch_combine(cp, s) != hipSuccess) return DORA_ERR_HIP;
+  }
   if (ev && hipEventRecord(ev[2], s) != hipSuccess) return DORA_ERR_HIP;
-  CombineParams cp{pp.seqinfo, dp.part_o, dp.part_ml, (uint16_t*)out, d.num_seqs,
-                   d.num_q_heads, d.num_kv_heads, G, d.head_dim};
-  if (launch_combine(cp, s) != hipSuccess) return DORA_ERR_HIP;
-  if (ev && hipEventRecord(ev[3], s) != hipSuccess) return DORA_ERR_HIP;
   return DORA_OK;
 }
 

@@ -1,31 +1,43 @@
-// Split-KV decode attention over a paged, multi-version KV pool, for gfx950.
+// Decode attention over a paged, multi-version KV pool, for gfx950.
 //
 // The operation is scaled dot-product attention of one decode query per head
 // over a sequence's cached tokens (the per-token decode step whose time enters
 // the paper's step-time model, Sec. 2.2 Eq. (1); sequences of several policy
 // versions share one pool, Sec. 3.2).  Decode is memory-bound (Sec. 1,
-// Sec. 2.2), so the kernels are built around streaming every K/V byte once:
+// Sec. 2.2) and the batch is long-tailed (Sec. 2.2, "Workload skewness"), so
+// the kernels stream every K/V byte exactly once and give every wavefront the
+// same number of bytes whatever the length mix:
 //
-//   plan     one workgroup: pages per split C from the batch's total pages,
-//            per-sequence split counts and partial-slot bases, and a work list
-//            ordered longest-first (counting sort on split size).
-//   split    one wavefront per (sequence, KV head, split).  The G query heads
-//            of the KV head are packed into the 16 columns of MFMA tiles, so
-//            each K/V byte is read once for the whole group:
+//   decode   stream-K over the flattened work list.  The work is the sequence
+//            of (sequence b, KV head g, page j) "page-heads", ordered by b,
+//            then g, then j; a segment is the run of pages of one (b, g).
+//            Every wavefront first computes the page prefix of the batch
+//            itself (no separate plan launch), then takes the contiguous range
+//            [w*T/W, (w+1)*T/W) of the T page-heads.  A segment that lies
+//            inside one range is finished in place; only the first and the
+//            last segment of a range can be cut, so each wavefront writes at
+//            most two partial results (unnormalised output, running max and
+//            sum), to slots 2w and 2w+1.
+//            Per page, the G query heads of the KV head are packed into the 16
+//            columns of MFMA tiles, so each K/V byte is read once per group:
 //              S^T[16 tok x 16 head] = K[16 tok x d] * Q^T   (mfma 16x16x32 bf16)
 //              O^T[16 d x 16 head]  += V^T[16 d x tok] * P^T  (mfma 16x16x{16,32} bf16)
 //            The page layouts (K: 16-byte head-dim chunks, token-major inside a
 //            chunk; V: tokens contiguous per head-dim index) make every lane's
-//            global load land directly in its MFMA operand registers, so pages
-//            stream HBM -> VGPRs with no LDS round trip; the next page is in
+//            global load land directly in its MFMA operand registers: pages
+//            stream HBM -> VGPRs with no LDS round trip, with the next pages in
 //            flight while the current one is consumed.  Online softmax in the
-//            log2 domain; max and sum reductions across the four 16-lane rows
-//            use cross-lane shuffles.  fp8 (OCP E4M3FN) pages are converted to
-//            bf16 in registers (exact) and the per-page scales are folded into
-//            the scores (K) and the probabilities (V).
-//   combine  log-sum-exp merge of the partial results of split sequences.
+//            log2 domain; max and sum reductions across the four 16-lane row
+//            groups use cross-lane shuffles.  fp8 (OCP E4M3FN) pages are
+//            converted to bf16 in registers (exact) and the per-page scales are
+//            folded into the scores (K) and the probabilities (V).
+//   combine  one workgroup per (b, g): zero output for an empty sequence, and
+//            for a segment that spans several ranges the log-sum-exp merge of
+//            their partial results.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "dora_internal.h"
 
@@ -39,126 +51,57 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------------------
-// plan
+// shared helpers
 // ---------------------------------------------------------------------------
 
 __device__ __forceinline__ int pages_of(int L, int P, int stride) {
   if (L <= 0) return 0;
-  int n = (L + P - 1) / P;
+  const int n = (L + P - 1) / P;
   return n < stride ? n : stride;  // a contract violation stays in bounds
 }
 
-// Inclusive block-wide prefix sum over kPlanThreads ints (Hillis-Steele).
-__device__ int block_inclusive_scan(int v, int* sh) {
-  const int t = threadIdx.x;
-  sh[t] = v;
-  __syncthreads();
-  for (int off = 1; off < kPlanThreads; off <<= 1) {
-    int add = t >= off ? sh[t - off] : 0;
-    __syncthreads();
-    sh[t] += add;
-    __syncthreads();
+__device__ __forceinline__ int wave_inclusive_scan(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(v, off);
+    if (lane >= off) v += y;
   }
-  int r = sh[t];
-  __syncthreads();
-  return r;
+  return v;
 }
 
-__global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanParams p) {
-  __shared__ long long red[kPlanThreads / 64];
-  __shared__ int scan[kPlanThreads];
-  __shared__ int hist[kPlanBins];
-  __shared__ int cursor[kPlanBins];
-  __shared__ int s_chunk;
-  __shared__ int s_tile;
-  const int t = threadIdx.x;
-  const int B = p.num_seqs, P = p.page_size;
+// Work range of wavefront w: [range_begin(w), range_begin(w + 1)).
+__device__ __forceinline__ int64_t range_begin(int64_t w, int64_t T, int64_t W) {
+  return w * T / W;
+}
 
-  // 1. total pages of the batch
-  long long local = 0;
-  for (int b = t; b < B; b += kPlanThreads) local += pages_of(p.seq_lens[b], P, p.stride);
-  for (int off = 32; off > 0; off >>= 1) local += __shfl_xor(local, off);
-  if ((t & 63) == 0) red[t >> 6] = local;
-  if (t < kPlanBins) hist[t] = 0;
-  __syncthreads();
-  if (t == 0) {
-    long long total = 0;
-    for (int w = 0; w < kPlanThreads / 64; ++w) total += red[w];
-    long long c;
-    if (p.force_pages > 0) {
-      c = p.force_pages;
-    } else {
-      long long work = total * p.num_kv_heads;
-      c = (work + p.target_units - 1) / p.target_units;
-      if (c < p.min_pages) c = p.min_pages;
-    }
-    if (c > 0x3fffffff) c = 0x3fffffff;
-    s_chunk = (int)c;
-  }
-  __syncthreads();
-  const int C = s_chunk;
+// Number of wavefronts that take part: at most the launched count, and few
+// enough that every range holds at least min_range (>= 1) page-heads, so no
+// range is empty (W <= T).
+__device__ __forceinline__ int64_t effective_waves(int64_t T, int64_t launched,
+                                                   int64_t min_range) {
+  const int64_t want = (T + min_range - 1) / min_range;
+  return want < launched ? (want > 0 ? want : 1) : launched;
+}
 
-  // 2. splits per sequence, their partial-slot bases, and a size histogram
-  int carry = 0;
-  for (int base = 0; base < B; base += kPlanThreads) {
-    const int b = base + t;
-    int n = 0, ns = 0;
-    if (b < B) {
-      n = pages_of(p.seq_lens[b], P, p.stride);
-      ns = n == 0 ? 1 : (n + C - 1) / C;
-    }
-    int incl = block_inclusive_scan(ns, scan);
-    if (b < B) {
-      p.seqinfo[b] = make_int2(carry + incl - ns, ns);
-      int last = n - (ns - 1) * C;  // pages of the final split (0 for an empty sequence)
-      if (ns > 1) atomicAdd(&hist[0], ns - 1);
-      atomicAdd(&hist[(int)((long long)(C - last) * (kPlanBins - 1) / C)], 1);
-    }
-    if (t == kPlanThreads - 1) s_tile = incl;  // splits in this tile of sequences
-    __syncthreads();
-    carry += s_tile;
-    __syncthreads();
-  }
-  // 3. bins in order of decreasing split size -> first work-list position
-  if (t == 0) {
-    int acc = 0;
-    for (int i = 0; i < kPlanBins; ++i) {
-      cursor[i] = acc;
-      acc += hist[i];
-    }
-    p.hdr[0] = acc;
-    p.hdr[1] = C;
-  }
-  __syncthreads();
-  // 4. scatter the work items
-  for (int b = t; b < B; b += kPlanThreads) {
-    const int n = pages_of(p.seq_lens[b], P, p.stride);
-    const int2 si = p.seqinfo[b];
-    const int ns = si.y;
-    if (ns > 1) {
-      int pos = atomicAdd(&cursor[0], ns - 1);
-      for (int s = 0; s < ns - 1; ++s)
-        p.items[pos + s] = make_int4(b, s * C, (s + 1) * C, si.x + s);
-    }
-    const int last = n - (ns - 1) * C;
-    int pos = atomicAdd(&cursor[(int)((long long)(C - last) * (kPlanBins - 1) / C)], 1);
-    p.items[pos] = make_int4(b, (ns - 1) * C, n, ns > 1 ? si.x + ns - 1 : -1);
-  }
+// Wavefront whose range holds page-head x: the largest w with begin(w) <= x.
+__device__ __forceinline__ int64_t wave_of(int64_t x, int64_t T, int64_t W) {
+  return ((x + 1) * W - 1) / T;
 }
 
 // ---------------------------------------------------------------------------
-// split decode
+// decode
 // ---------------------------------------------------------------------------
 
 // Raw bytes of one page's K and V tiles for one KV head, as each lane loads them.
 template <int D, int P, bool FP8>
 struct PageRegs {
-  static constexpr int NT = P / 16;                         // 16-token sub-tiles
+  static constexpr int NT = P / 16;                               // 16-token sub-tiles
   static constexpr int NK = FP8 ? NT * (D / 64) : NT * (D / 32);  // 16-byte K loads
-  static constexpr int VB = (P == 16 ? 4 : 8) * (FP8 ? 1 : 2);   // bytes per V load
+  static constexpr int VB = (P == 16 ? 4 : 8) * (FP8 ? 1 : 2);    // bytes per V load
   u32x4 k[NK];
-  typedef typename std::conditional<VB == 16, u32x4,
-          typename std::conditional<VB == 8, u32x2, uint32_t>::type>::type vraw_t;
+  typedef typename std::conditional<
+      VB == 16, u32x4, typename std::conditional<VB == 8, u32x2, uint32_t>::type>::type vraw_t;
   vraw_t v[D / 16];
 };
 
@@ -171,16 +114,16 @@ __device__ __forceinline__ int tile_token(int t, int r) {
 }
 
 __device__ __forceinline__ bf16x8 fp8x8_to_bf16(uint32_t w0, uint32_t w1) {
-  bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, false);
-  bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, true);
-  bf16x2 c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w1, 1.0f, false);
-  bf16x2 d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w1, 1.0f, true);
+  const bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, false);
+  const bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, true);
+  const bf16x2 c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w1, 1.0f, false);
+  const bf16x2 d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w1, 1.0f, true);
   return bf16x8{a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
 }
 
 __device__ __forceinline__ bf16x4 fp8x4_to_bf16(uint32_t w0) {
-  bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, false);
-  bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, true);
+  const bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, false);
+  const bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, true);
   return bf16x4{a[0], a[1], b[0], b[1]};
 }
 
@@ -197,242 +140,386 @@ __device__ __forceinline__ void load_page(PageRegs<D, P, FP8>& r, const uint8_t*
     r.v[i] = *(const typename R::vraw_t*)(vbase + voff + i * vrow);
 }
 
-template <int D, int P, bool FP8>
-__global__ __launch_bounds__(64) void split_decode_kernel(DecodeParams p) {
+// Page-head descriptor word: j (19 bits) | g << 19 (7 bits) | last << 26 |
+// (tokens valid in the page - 1) << 27.
+__device__ __forceinline__ int desc_j(uint32_t d) { return (int)(d & 0x7FFFFu); }
+__device__ __forceinline__ int desc_g(uint32_t d) { return (int)((d >> 19) & 0x7Fu); }
+__device__ __forceinline__ bool desc_last(uint32_t d) { return (d >> 26) & 1u; }
+__device__ __forceinline__ int desc_nvalid(uint32_t d) { return (int)(d >> 27) + 1; }
+
+template <int D, int P, bool FP8, int NBUF>
+__global__ __launch_bounds__(64) void decode_kernel(DecodeParams p) {
   typedef PageRegs<D, P, FP8> R;
   constexpr int NT = R::NT;
   constexpr int KSTEPS = D / 32;
   constexpr int DBLK = D / 16;
   constexpr int E = FP8 ? 1 : 2;
   constexpr int TILE_BYTES = P * D * E;  // one KV head of one page
+  extern __shared__ int sN[];            // page prefix over sequences, [B + 1]
 
   const int lane = threadIdx.x;
   const int col = lane & 15;  // MFMA row/column index of this lane
   const int grp = lane >> 4;  // 16-lane row group
-  const int Hkv = p.num_kv_heads;
-  const int u = blockIdx.x / Hkv;
-  const int g = blockIdx.x - u * Hkv;
-  if (u >= p.hdr[0]) return;
-  const int4 it = p.items[u];
-  const int b = it.x, j0 = it.y, j1 = it.z, slot = it.w;
-  const int L = p.seq_lens[b];
-  const int G = p.group;
-  const int Hq = p.num_q_heads;
+  const int B = p.num_seqs, Hkv = p.num_kv_heads, G = p.group, Hq = p.num_q_heads;
 
-  f32x4 acc[DBLK];
+  // 1. page prefix N(b) = pages of the sequences before b, in LDS
+  int carry = 0;
+  for (int base = 0; base < B; base += 64 * 8) {
+    int n[8], tsum = 0;
 #pragma unroll
-  for (int i = 0; i < DBLK; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -__builtin_inff();
-  float l_run = 0.f;
+    for (int k = 0; k < 8; ++k) {
+      const int b = base + lane * 8 + k;
+      n[k] = b < B ? pages_of(p.seq_lens[b], P, p.stride) : 0;
+      tsum += n[k];
+    }
+    const int incl = wave_inclusive_scan(tsum);
+    int excl = carry + incl - tsum;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int b = base + lane * 8 + k;
+      if (b < B) sN[b] = excl;
+      excl += n[k];
+    }
+    carry += __shfl(incl, 63);
+  }
+  if (lane == 0) sN[B] = carry;
+  __syncthreads();
+  if (blockIdx.x == 0)  // the combine kernel reads the prefix back
+    for (int b = lane; b <= B; b += 64) p.prefix[b] = sN[b];
 
-  if (j1 > j0) {
+  // 2. this wavefront's range of page-heads
+  const int64_t T = (int64_t)Hkv * carry;
+  const int64_t W = effective_waves(T, gridDim.x, p.min_range);
+  const int64_t w = blockIdx.x;
+  if (T == 0 || w >= W) return;
+  const int64_t x0 = range_begin(w, T, W), x1 = range_begin(w + 1, T, W);
+
+  // Descriptors of 64 consecutive page-heads, one per lane: sequence, page id,
+  // packed (j, g, last, valid tokens).
+  auto describe = [&](int64_t cbase, int& db, int& dpid, uint32_t& dinfo) {
+    const int64_t x = cbase + lane;
+    db = 0;
+    dpid = 0;
+    dinfo = 0;
+    if (x < x1) {
+      int lo = 0, hi = B;  // largest b with Hkv * N(b) <= x
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if ((int64_t)Hkv * sN[mid] <= x) lo = mid; else hi = mid;
+      }
+      const int nb = sN[lo + 1] - sN[lo];
+      const int r = (int)(x - (int64_t)Hkv * sN[lo]);
+      const int g = r / nb;
+      const int j = r - g * nb;
+      int nv = p.seq_lens[lo] - j * P;
+      nv = nv > P ? P : nv;
+      db = lo;
+      dpid = p.block_table[(int64_t)lo * p.stride + j];
+      dinfo = (uint32_t)j | ((uint32_t)g << 19) | ((uint32_t)(j == nb - 1) << 26) |
+              ((uint32_t)(nv - 1) << 27);
+    }
+  };
+
+  // Per-lane byte offsets inside a (page, KV head) tile.
+  uint32_t koff[R::NK];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int tok = tile_token<P>(t, col);
+    constexpr int per_t = R::NK / NT;
+#pragma unroll
+    for (int s = 0; s < per_t; ++s) koff[t * per_t + s] = ((4 * s + grp) * P + tok) * 16;
+  }
+  const uint32_t voff = (uint32_t)((col * P + (P == 16 ? 4 : 8) * grp) * E);
+  const int64_t pb = p.page_bytes;
+
+  // running state of the current segment
+  f32x4 acc[DBLK];
+  bf16x8 qop[KSTEPS];
+  float m_run = -__builtin_inff(), l_run = 0.f;
+  int seg_b = 0, seg_g = 0;
+  bool seg_whole = false, first_seg = true;
+
+  auto start_segment = [&](int b, int g, bool whole) {
+    seg_b = b;
+    seg_g = g;
+    seg_whole = whole;
+    m_run = -__builtin_inff();
+    l_run = 0.f;
+#pragma unroll
+    for (int i = 0; i < DBLK; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     // Query operand: lane supplies q[head col][8 head-dim values] per k-step.
-    bf16x8 qop[KSTEPS];
     const uint16_t* qrow = p.q + ((int64_t)b * Hq + (int64_t)g * G + col) * D;
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
       const int dst = FP8 ? 64 * (s >> 1) + 16 * grp + 8 * (s & 1) : 32 * s + 8 * grp;
-      if (col < G)
-        qop[s] = *(const bf16x8*)(qrow + dst);
-      else
-        qop[s] = bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      qop[s] = col < G ? *(const bf16x8*)(qrow + dst) : bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
     }
-    // Per-lane byte offsets inside a (page, KV head) tile.
-    uint32_t koff[R::NK];
+  };
+
+  auto finish_segment = [&]() {
+    // Sum of exponentials over the four row groups (same head, other tokens).
+    float l_tot = l_run + __shfl_xor(l_run, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    if (col < G) {
+      if (seg_whole) {
+        const float inv = 1.f / l_tot;
+        uint16_t* o = p.out + ((int64_t)seg_b * Hq + seg_g * G + col) * D + 4 * grp;
+#pragma unroll
+        for (int i = 0; i < DBLK; ++i)
+          *(bf16x4*)(o + 16 * i) =
+              bf16x4{(__bf16)(acc[i][0] * inv), (__bf16)(acc[i][1] * inv),
+                     (__bf16)(acc[i][2] * inv), (__bf16)(acc[i][3] * inv)};
+      } else {
+        const int64_t slot = 2 * w + (first_seg ? 0 : 1);
+        float* po = p.part_o + (slot * G + col) * D + 4 * grp;
+#pragma unroll
+        for (int i = 0; i < DBLK; ++i) *(f32x4*)(po + 16 * i) = acc[i];
+        if (grp == 0) p.part_ml[slot * G + col] = make_float2(m_run, l_tot);
+      }
+    }
+    first_seg = false;
+  };
+
+  auto consume = [&](const R& r, int nvalid, float ksc, float vsc) {
+    // scores S^T: lane holds tokens of its row group for head `col`
+    f32x4 sc[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      const int tok = tile_token<P>(t, col);
-      constexpr int per_t = R::NK / NT;
+      f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < per_t; ++s) koff[t * per_t + s] = ((4 * s + grp) * P + tok) * 16;
+      for (int ks = 0; ks < KSTEPS; ++ks) {
+        bf16x8 a;
+        if constexpr (FP8) {
+          const u32x4& wd = r.k[t * (D / 64) + (ks >> 1)];
+          a = (ks & 1) ? fp8x8_to_bf16(wd[2], wd[3]) : fp8x8_to_bf16(wd[0], wd[1]);
+        } else {
+          a = __builtin_bit_cast(bf16x8, r.k[t * KSTEPS + ks]);
+        }
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[ks], s, 0, 0, 0);
+      }
+      sc[t] = s;
     }
-    const uint32_t voff = (uint32_t)((col * P + (P == 16 ? 4 : 8) * grp) * E);
+    float mx = -__builtin_inff();
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float x = sc[t][i] * ksc;
+        const int tok = P == 16 ? 4 * grp + i : 8 * grp + 4 * t + i;
+        if (nvalid < P && tok >= nvalid) x = -__builtin_inff();
+        sc[t][i] = x;
+        mx = fmaxf(mx, x);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float e = __builtin_amdgcn_exp2f(sc[t][i] - m_new);
+        psum += e;
+        sc[t][i] = e * vsc;
+      }
+    l_run = l_run * alpha + psum;
+    if (__ballot(alpha != 1.f)) {
+#pragma unroll
+      for (int i = 0; i < DBLK; ++i) acc[i] *= alpha;
+    }
+    // P^T operand, then O^T += V^T P^T per 16-row block of the head dim
+    if constexpr (P == 16) {
+      const bf16x4 pb4 = bf16x4{(__bf16)sc[0][0], (__bf16)sc[0][1], (__bf16)sc[0][2],
+                                (__bf16)sc[0][3]};
+#pragma unroll
+      for (int i = 0; i < DBLK; ++i) {
+        bf16x4 a;
+        if constexpr (FP8)
+          a = fp8x4_to_bf16(r.v[i]);
+        else
+          a = __builtin_bit_cast(bf16x4, r.v[i]);
+        if (nvalid < P) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (4 * grp + e >= nvalid) a[e] = (__bf16)0.f;
+        }
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, pb4, acc[i], 0, 0, 0);
+      }
+    } else {
+      const bf16x8 pb8 = bf16x8{(__bf16)sc[0][0], (__bf16)sc[0][1], (__bf16)sc[0][2],
+                                (__bf16)sc[0][3], (__bf16)sc[1][0], (__bf16)sc[1][1],
+                                (__bf16)sc[1][2], (__bf16)sc[1][3]};
+#pragma unroll
+      for (int i = 0; i < DBLK; ++i) {
+        bf16x8 a;
+        if constexpr (FP8)
+          a = fp8x8_to_bf16(r.v[i][0], r.v[i][1]);
+        else
+          a = __builtin_bit_cast(bf16x8, r.v[i]);
+        if (nvalid < P) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (8 * grp + e >= nvalid) a[e] = (__bf16)0.f;
+        }
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb8, acc[i], 0, 0, 0);
+      }
+    }
+  };
 
-    const int32_t* bt = p.block_table + (int64_t)b * p.stride;
-    const uint8_t* kpool = p.k_pages + (int64_t)g * TILE_BYTES;
-    const uint8_t* vpool = p.v_pages + (int64_t)g * TILE_BYTES;
-    const int64_t pb = p.page_bytes;
+  // 3. stream the range.  Descriptors come in chunks of 64 (current and next);
+  // NBUF page buffers rotate so that NBUF-1 pages are in flight while one is
+  // consumed.  Past the end the last page-head is re-requested (a cache hit),
+  // so every iteration issues the same loads.
+  int cb_b, cb_pid, nb_b, nb_pid;
+  uint32_t cb_info, nb_info;
+  describe(x0, cb_b, cb_pid, cb_info);
+  describe(x0 + 64, nb_b, nb_pid, nb_info);
+  int64_t chunk = x0;  // first page-head of the current descriptor chunk
 
-    // Page ids are fetched 64 at a time with one vector load and read with
-    // readlane (wave-uniform), so no scalar-load latency sits in the loop.
-    int bt_base = j0;
-    int bt_vec = (j0 + lane < j1) ? bt[j0 + lane] : 0;
-    int bt_next = (j0 + 64 + lane < j1) ? bt[j0 + 64 + lane] : 0;
-    auto page_id = [&](int j) -> int {
-      if (j - bt_base >= 64) {
-        bt_base += 64;
-        bt_vec = bt_next;
-        bt_next = (bt_base + 64 + lane < j1) ? bt[bt_base + 64 + lane] : 0;
-      }
-      return __builtin_amdgcn_readlane(bt_vec, j - bt_base);
-    };
+  R buf[NBUF];
+  int s_b[NBUF];
+  uint32_t s_info[NBUF];
+  float s_ks[NBUF], s_vs[NBUF];
 
-    auto consume = [&](const R& r, int j, int pid) {
-      // scores S^T: lane holds tokens of its row group for head `col`
-      f32x4 sc[NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KSTEPS; ++ks) {
-          bf16x8 a;
-          if constexpr (FP8) {
-            const u32x4& w = r.k[t * (D / 64) + (ks >> 1)];
-            a = (ks & 1) ? fp8x8_to_bf16(w[2], w[3]) : fp8x8_to_bf16(w[0], w[1]);
-          } else {
-            a = __builtin_bit_cast(bf16x8, r.k[t * KSTEPS + ks]);
-          }
-          s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[ks], s, 0, 0, 0);
-        }
-        sc[t] = s;
-      }
-      float ksc = p.scale_log2;
-      float vsc = 1.f;
-      if constexpr (FP8) {
-        ksc *= p.k_scales[pid];
-        vsc = p.v_scales[pid];
-      }
-      const int nvalid = L - j * P;  // >= 1; < P only on a sequence's last page
-      float mx = -__builtin_inff();
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float x = sc[t][i] * ksc;
-          const int tok = P == 16 ? 4 * grp + i : 8 * grp + 4 * t + i;
-          if (nvalid < P && tok >= nvalid) x = -__builtin_inff();
-          sc[t][i] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      float psum = 0.f;
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float e = __builtin_amdgcn_exp2f(sc[t][i] - m_new);
-          psum += e;
-          sc[t][i] = e * vsc;
-        }
-      l_run = l_run * alpha + psum;
-      if (__ballot(alpha != 1.f)) {
-#pragma unroll
-        for (int i = 0; i < DBLK; ++i) acc[i] *= alpha;
-      }
-      // P^T operand, then O^T += V^T P^T per 16-row block of the head dim
-      if constexpr (P == 16) {
-        bf16x4 pb4 = bf16x4{(__bf16)sc[0][0], (__bf16)sc[0][1], (__bf16)sc[0][2],
-                            (__bf16)sc[0][3]};
-#pragma unroll
-        for (int i = 0; i < DBLK; ++i) {
-          bf16x4 a;
-          if constexpr (FP8)
-            a = fp8x4_to_bf16(r.v[i]);
-          else
-            a = __builtin_bit_cast(bf16x4, r.v[i]);
-          if (nvalid < P) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (4 * grp + e >= nvalid) a[e] = (__bf16)0.f;
-          }
-          acc[i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, pb4, acc[i], 0, 0, 0);
-        }
-      } else {
-        bf16x8 pb8 = bf16x8{(__bf16)sc[0][0], (__bf16)sc[0][1], (__bf16)sc[0][2],
-                            (__bf16)sc[0][3], (__bf16)sc[1][0], (__bf16)sc[1][1],
-                            (__bf16)sc[1][2], (__bf16)sc[1][3]};
-#pragma unroll
-        for (int i = 0; i < DBLK; ++i) {
-          bf16x8 a;
-          if constexpr (FP8)
-            a = fp8x8_to_bf16(r.v[i][0], r.v[i][1]);
-          else
-            a = __builtin_bit_cast(bf16x8, r.v[i]);
-          if (nvalid < P) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (8 * grp + e >= nvalid) a[e] = (__bf16)0.f;
-          }
-          acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb8, acc[i], 0, 0, 0);
-        }
-      }
-    };
+  auto prefetch = [&](int r, int64_t x) {
+    if (x >= x1) x = x1 - 1;
+    if (x - chunk >= 64) {
+      chunk += 64;
+      cb_b = nb_b;
+      cb_pid = nb_pid;
+      cb_info = nb_info;
+      describe(chunk + 64, nb_b, nb_pid, nb_info);
+    }
+    const int i = (int)(x - chunk);
+    const int b = __builtin_amdgcn_readlane(cb_b, i);
+    const int pid = __builtin_amdgcn_readlane(cb_pid, i);
+    const uint32_t info = (uint32_t)__builtin_amdgcn_readlane((int)cb_info, i);
+    s_b[r] = b;
+    s_info[r] = info;
+    const int64_t tile = (int64_t)pid * pb + (int64_t)desc_g(info) * TILE_BYTES;
+    if constexpr (FP8) {
+      s_ks[r] = p.k_scales[pid] * p.scale_log2;
+      s_vs[r] = p.v_scales[pid];
+    } else {
+      s_ks[r] = p.scale_log2;
+      s_vs[r] = 1.f;
+    }
+    load_page<D, P, FP8>(buf[r], p.k_pages + tile, p.v_pages + tile, koff, voff);
+  };
 
-    // Two register buffers; the load of page j+1 is issued before page j is
-    // consumed.  Past the end the last page is re-requested (a cache hit) so
-    // that every iteration issues the same loads.
-    R ra, rb;
-    int pid_a = page_id(j0);
-    load_page<D, P, FP8>(ra, kpool + (int64_t)pid_a * pb, vpool + (int64_t)pid_a * pb, koff,
-                         voff);
-    int j = j0;
-    while (true) {
-      const int pid_b = page_id(min(j + 1, j1 - 1));
-      load_page<D, P, FP8>(rb, kpool + (int64_t)pid_b * pb, vpool + (int64_t)pid_b * pb, koff,
-                           voff);
-      consume(ra, j, pid_a);
-      if (++j >= j1) break;
-      pid_a = page_id(min(j + 1, j1 - 1));
-      load_page<D, P, FP8>(ra, kpool + (int64_t)pid_a * pb, vpool + (int64_t)pid_a * pb, koff,
-                           voff);
-      consume(rb, j, pid_b);
-      if (++j >= j1) break;
+#pragma unroll
+  for (int k = 0; k < NBUF - 1; ++k) prefetch(k, x0 + k);
+  int64_t x = x0;
+  while (true) {
+#pragma unroll
+    for (int r = 0; r < NBUF; ++r) {
+      prefetch((r + NBUF - 1) % NBUF, x + NBUF - 1);
+      const uint32_t info = s_info[r];
+      const int j = desc_j(info);
+      if (x == x0 || j == 0) start_segment(s_b[r], desc_g(info), j == 0);
+      consume(buf[r], desc_nvalid(info), s_ks[r], s_vs[r]);
+      if (desc_last(info) || x == x1 - 1) {
+        seg_whole = seg_whole && desc_last(info);
+        finish_segment();
+      }
+      if (++x >= x1) goto done;
     }
   }
-
-  // Sum of exponentials over the four row groups (same head, other tokens).
-  float l_tot = l_run + __shfl_xor(l_run, 16);
-  l_tot += __shfl_xor(l_tot, 32);
-  if (col >= G) return;
-  const int h = g * G + col;
-  if (slot < 0) {
-    const float inv = j1 > j0 ? 1.f / l_tot : 0.f;
-    uint16_t* o = p.out + ((int64_t)b * Hq + h) * D + 4 * grp;
-#pragma unroll
-    for (int i = 0; i < DBLK; ++i) {
-      bf16x4 v = bf16x4{(__bf16)(acc[i][0] * inv), (__bf16)(acc[i][1] * inv),
-                        (__bf16)(acc[i][2] * inv), (__bf16)(acc[i][3] * inv)};
-      *(bf16x4*)(o + 16 * i) = v;
-    }
-  } else {
-    float* po = p.part_o + (((int64_t)slot * Hkv + g) * G + col) * D + 4 * grp;
-#pragma unroll
-    for (int i = 0; i < DBLK; ++i) *(f32x4*)(po + 16 * i) = acc[i];
-    if (grp == 0) p.part_ml[((int64_t)slot * Hkv + g) * G + col] = make_float2(m_run, l_tot);
-  }
+done:;
 }
 
 // ---------------------------------------------------------------------------
-// combine: out = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s
+// combine
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
+constexpr int kCombineThreads = 1024;
+
+// Merge (M, S) with (m, l): S is a sum of 2^(x - M) terms.
+__device__ __forceinline__ void lse_merge(float& M, float& S, float m, float l) {
+  if (m > M) {
+    S = S * __builtin_amdgcn_exp2f(M - m) + l;
+    M = m;
+  } else if (m > -__builtin_inff()) {
+    S += l * __builtin_amdgcn_exp2f(m - M);
+  }
+}
+
+// One workgroup per (sequence, KV head).  Pass 1: the per-head max and
+// normaliser over the partials (one online pass, merged in LDS).  Pass 2: the
+// weighted sum of the partial outputs by (head, 4 head-dim values) tasks x
+// partial groups, the groups summed in LDS.  The k-th wavefront holding part
+// of the segment is wa + k; wa's partial is in slot 2wa + 1 unless its range
+// starts exactly at the segment (then slot 2wa), every later one's in 2w.
+__global__ __launch_bounds__(kCombineThreads) void combine_kernel(CombineParams p) {
+  __shared__ float sM[kCombineThreads], sS[kCombineThreads];
+  __shared__ f32x4 sAcc[kCombineThreads];
   const int Hkv = p.num_kv_heads;
   const int b = blockIdx.x / Hkv;
   const int g = blockIdx.x - b * Hkv;
-  const int2 si = p.seqinfo[b];
-  const int ns = si.y;
-  if (ns <= 1) return;
+  const int t = threadIdx.x;
   const int G = p.group, D = p.head_dim;
-  const int64_t split_stride = (int64_t)Hkv * G;
-  for (int e = threadIdx.x; e < G * D; e += blockDim.x) {
-    const int n = e / D, d = e - n * D;
-    const int64_t r0 = ((int64_t)si.x * Hkv + g) * G + n;
-    float M = -__builtin_inff();
-    for (int s = 0; s < ns; ++s) M = fmaxf(M, p.part_ml[r0 + s * split_stride].x);
-    float den = 0.f, num = 0.f;
-    for (int s = 0; s < ns; ++s) {
-      const float2 ml = p.part_ml[r0 + s * split_stride];
-      const float w = __builtin_amdgcn_exp2f(ml.x - M);
-      den += w * ml.y;
-      num += w * p.part_o[(r0 + s * split_stride) * D + d];
+  const int Nb = p.prefix[b], nb = p.prefix[b + 1] - Nb;
+  if (nb == 0) {  // empty sequence: zero output
+    for (int e = t; e < G * D; e += kCombineThreads)
+      p.out[((int64_t)b * p.num_q_heads + g * G) * D + e] = 0;
+    return;
+  }
+  const int64_t T = (int64_t)Hkv * p.prefix[p.num_seqs];
+  const int64_t W = effective_waves(T, p.launched_waves, p.min_range);
+  const int64_t s0 = (int64_t)Hkv * Nb + (int64_t)g * nb;
+  const int64_t wa = wave_of(s0, T, W), wb = wave_of(s0 + nb - 1, T, W);
+  if (wa == wb) return;  // finished in place by the decode kernel
+  const int np = (int)(wb - wa + 1);
+  const int first_off = range_begin(wa, T, W) == s0 ? 0 : 1;
+  auto slot_of = [&](int k) -> int64_t { return 2 * (wa + k) + (k == 0 ? first_off : 0); };
+
+  {
+    const int n = t & 15, sl = t >> 4;
+    float M = -__builtin_inff(), S = 0.f;
+    if (n < G)
+      for (int k = sl; k < np; k += kCombineThreads / 16) {
+        const float2 ml = p.part_ml[slot_of(k) * G + n];
+        lse_merge(M, S, ml.x, ml.y);
+      }
+    sM[t] = M;
+    sS[t] = S;
+  }
+  __syncthreads();
+  for (int off = kCombineThreads / 2; off >= 16; off >>= 1) {
+    if (t < off) {
+      float M = sM[t], S = sS[t];
+      lse_merge(M, S, sM[t + off], sS[t + off]);
+      sM[t] = M;
+      sS[t] = S;
     }
-    const __bf16 v = (__bf16)(num / den);
-    p.out[((int64_t)b * p.num_q_heads + g * G + n) * D + d] = __builtin_bit_cast(uint16_t, v);
+    __syncthreads();
+  }
+  const int tasks = G * (D / 4);
+  const int tasks_r = (tasks + 63) & ~63;
+  const int groups = kCombineThreads / tasks_r;  // >= 2 since tasks <= 512
+  const int task = t % tasks_r, sg = t / tasks_r;
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (task < tasks && sg < groups) {
+    const int n = task / (D / 4), d4 = task - n * (D / 4);
+    const float M = sM[n];
+    for (int k = sg; k < np; k += groups) {
+      const int64_t row = slot_of(k) * G + n;
+      const float wgt = __builtin_amdgcn_exp2f(p.part_ml[row].x - M);
+      const f32x4 o = *(const f32x4*)(p.part_o + row * D + 4 * d4);
+      acc += wgt * o;
+    }
+  }
+  sAcc[t] = acc;
+  __syncthreads();
+  if (sg == 0 && task < tasks) {
+    for (int k = 1; k < groups; ++k) acc += sAcc[k * tasks_r + task];
+    const int n = task / (D / 4), d4 = task - n * (D / 4);
+    const float inv = 1.f / sS[n];
+    uint16_t* o = p.out + ((int64_t)b * p.num_q_heads + g * G + n) * D + 4 * d4;
+    *(bf16x4*)o = bf16x4{(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv),
+                         (__bf16)(acc[2] * inv), (__bf16)(acc[3] * inv)};
   }
 }
 
@@ -468,36 +555,47 @@ __global__ void fill_i32_kernel(int32_t* dst, int32_t value, int64_t n) {
 // launchers
 // ---------------------------------------------------------------------------
 
-hipError_t launch_plan(const PlanParams& p, hipStream_t s) {
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, s, p);
-  return hipGetLastError();
+// Register buffers per wave: two pages in flight where the register budget
+// keeps two waves per SIMD, one page otherwise.
+template <int D, int P, bool FP8>
+constexpr int page_buffers() {
+  return (P == 32 && !FP8 && D == 128) ? 2 : 3;
 }
 
 template <int D, int P, bool FP8>
-static hipError_t launch_split_t(const DecodeParams& p, int64_t grid, hipStream_t s) {
-  hipLaunchKernelGGL((split_decode_kernel<D, P, FP8>), dim3((unsigned)grid), dim3(64), 0, s, p);
-  return hipGetLastError();
+static const void* decode_fn() {
+  return (const void*)&decode_kernel<D, P, FP8, page_buffers<D, P, FP8>()>;
 }
 
-hipError_t launch_split_decode(const DecodeParams& p, int head_dim, int page_size, bool fp8,
-                               int64_t grid, hipStream_t s) {
-  if (grid <= 0) return hipSuccess;
+static const void* decode_symbol(int head_dim, int page_size, bool fp8) {
   if (head_dim == 128) {
-    if (page_size == 16) return fp8 ? launch_split_t<128, 16, true>(p, grid, s)
-                                    : launch_split_t<128, 16, false>(p, grid, s);
-    return fp8 ? launch_split_t<128, 32, true>(p, grid, s)
-               : launch_split_t<128, 32, false>(p, grid, s);
+    if (page_size == 16) return fp8 ? decode_fn<128, 16, true>() : decode_fn<128, 16, false>();
+    return fp8 ? decode_fn<128, 32, true>() : decode_fn<128, 32, false>();
   }
-  if (page_size == 16) return fp8 ? launch_split_t<64, 16, true>(p, grid, s)
-                                  : launch_split_t<64, 16, false>(p, grid, s);
-  return fp8 ? launch_split_t<64, 32, true>(p, grid, s)
-             : launch_split_t<64, 32, false>(p, grid, s);
+  if (page_size == 16) return fp8 ? decode_fn<64, 16, true>() : decode_fn<64, 16, false>();
+  return fp8 ? decode_fn<64, 32, true>() : decode_fn<64, 32, false>();
+}
+
+size_t decode_lds_bytes(int num_seqs) { return (size_t)(num_seqs + 1) * sizeof(int); }
+
+hipError_t decode_waves_per_cu(int head_dim, int page_size, bool fp8, int num_seqs, int* out) {
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(
+      out, decode_symbol(head_dim, page_size, fp8), 64, decode_lds_bytes(num_seqs));
+}
+
+hipError_t launch_decode(const DecodeParams& p, int head_dim, int page_size, bool fp8,
+                         int64_t waves, hipStream_t s) {
+  if (waves <= 0) return hipSuccess;
+  DecodeParams arg = p;
+  void* args[] = {(void*)&arg};
+  return hipLaunchKernel(decode_symbol(head_dim, page_size, fp8), dim3((unsigned)waves),
+                         dim3(64), args, decode_lds_bytes(p.num_seqs), s);
 }
 
 hipError_t launch_combine(const CombineParams& p, hipStream_t s) {
   const int64_t grid = (int64_t)p.num_seqs * p.num_kv_heads;
   if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL(combine_kernel, dim3((unsigned)grid), dim3(256), 0, s, p);
+  hipLaunchKernelGGL(combine_kernel, dim3((unsigned)grid), dim3(kCombineThreads), 0, s, p);
   return hipGetLastError();
 }
 

@@ -10,40 +10,32 @@
 
 namespace dora {
 
-// Default target number of (sequence, KV head, split) work units per call: 16
-// units per compute unit of a 256-CU device, enough for the grid's tail to be
-// a small fraction of the call even when one sequence holds most of the pages.
-constexpr int kDefaultTargetUnits = 4096;
-// Smallest split (pages) chosen automatically: a split must carry enough bytes
-// to amortise its start-up latency and its partial-result write.
-constexpr int kMinSplitPages = 4;
-// Threads of the single-workgroup plan kernel.
-constexpr int kPlanThreads = 1024;
-// Size-ordering bins of the plan kernel (longest work units dispatched first).
-constexpr int kPlanBins = 256;
-// Bytes reserved at the start of the workspace for plan counters / flags.
+// Default number of decode wavefronts per resident wavefront slot (compute
+// units x occupancy): one equal range per slot.
+constexpr int kWaveFactor = 1;
+// Smallest range (page-heads) a wavefront gets by default: a range must carry
+// enough bytes to amortise the wavefront's start-up (page prefix, first loads).
+constexpr int kMinRangePages = 8;
+// Largest batch one decode launch takes: its page prefix ((B + 1) ints) lives
+// in each wavefront's LDS.  Larger batches are cut into launches of this size.
+constexpr int kMaxSeqsPerLaunch = 8192;
+// Bytes reserved at the start of the workspace for flags.
 constexpr size_t kWsHeaderBytes = 256;
 
 // Workspace carve-up for one geometry (offsets in bytes from the base).
 struct WsLayout {
-  int64_t max_items;   // upper bound on (sequence, split) items
-  size_t seqinfo_off;  // int2 [B]      {first partial slot, number of splits}
-  size_t items_off;    // int4 [max_items] {b, first page, end page, slot or -1}
-  size_t part_o_off;   // float [max_items][Hkv][G][D] unnormalised partial outputs
-  size_t part_ml_off;  // float2 [max_items][Hkv][G] {running max (log2 units), sum}
+  int64_t waves;       // decode wavefronts launched (2 partial slots each)
+  size_t prefix_off;   // int32 [min(B, kMaxSeqsPerLaunch) + 1] page prefix
+  size_t part_o_off;   // float [2 * waves][G][D] unnormalised partial outputs
+  size_t part_ml_off;  // float2 [2 * waves][G] {running max (log2 units), sum}
   size_t total;
 };
 
-bool ws_layout(const dora_decode_desc& d, WsLayout* out);
-
-struct PlanParams {
-  const int32_t* seq_lens;
-  int32_t num_seqs, page_size, num_kv_heads, stride;
-  int32_t target_units, min_pages, force_pages;
-  int32_t* hdr;        // hdr[0] = number of items, hdr[1] = pages per split
-  int2* seqinfo;
-  int4* items;
-};
+// Decode wavefronts to launch for this descriptor on the current device
+// (desc->num_waves if set).  Falls back to a 256-CU, 8-wave estimate when no
+// device can be queried.
+int64_t decode_waves(const dora_decode_desc& d);
+bool ws_layout(const dora_decode_desc& d, int64_t waves, WsLayout* out);
 
 struct DecodeParams {
   const uint16_t* q;
@@ -54,21 +46,23 @@ struct DecodeParams {
   const int32_t* block_table;
   const int32_t* seq_lens;
   uint16_t* out;
-  const int32_t* hdr;
-  const int4* items;
+  int32_t* prefix;     // written by wavefront 0: page prefix [B + 1]
   float* part_o;
   float2* part_ml;
-  int32_t num_q_heads, num_kv_heads, group, stride;
+  int32_t num_seqs, num_q_heads, num_kv_heads, group, stride;
+  int32_t min_range;   // smallest range in page-heads
   int64_t page_bytes;  // bytes of one K (or V) page, all KV heads
   float scale_log2;    // softmax scale times log2(e)
 };
 
 struct CombineParams {
-  const int2* seqinfo;
+  const int32_t* prefix;
   const float* part_o;
   const float2* part_ml;
   uint16_t* out;
   int32_t num_seqs, num_q_heads, num_kv_heads, group, head_dim;
+  int32_t min_range;
+  int64_t launched_waves;
 };
 
 struct ValidateParams {
@@ -81,9 +75,10 @@ struct ValidateParams {
   int32_t* err;
 };
 
-hipError_t launch_plan(const PlanParams& p, hipStream_t s);
-hipError_t launch_split_decode(const DecodeParams& p, int head_dim, int page_size, bool fp8,
-                               int64_t grid, hipStream_t s);
+size_t decode_lds_bytes(int num_seqs);
+hipError_t decode_waves_per_cu(int head_dim, int page_size, bool fp8, int num_seqs, int* out);
+hipError_t launch_decode(const DecodeParams& p, int head_dim, int page_size, bool fp8,
+                         int64_t waves, hipStream_t s);
 hipError_t launch_combine(const CombineParams& p, hipStream_t s);
 hipError_t launch_validate(const ValidateParams& p, hipStream_t s);
 hipError_t launch_fill_i32(int32_t* dst, int32_t value, int64_t n, hipStream_t s);

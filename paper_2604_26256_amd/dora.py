@@ -31,7 +31,6 @@ DORA_ERR_NOT_FOUND = 8
 DORA_KV_BF16 = 0
 DORA_KV_FP8_E4M3 = 1
 DORA_FLAG_VALIDATE = 0x1
-DORA_FLAG_FORCE_SPLIT = 0x2
 
 
 class DoraError(RuntimeError):
@@ -48,8 +47,8 @@ class dora_decode_desc(ctypes.Structure):
         ("num_pages", ctypes.c_int64), ("kv_dtype", ctypes.c_int32),
         ("sm_scale", ctypes.c_float), ("k_scales", ctypes.c_void_p),
         ("v_scales", ctypes.c_void_p), ("page_owner", ctypes.c_void_p),
-        ("flags", ctypes.c_uint32), ("split_pages", ctypes.c_int32),
-        ("target_units", ctypes.c_int32), ("prof_events", ctypes.c_void_p),
+        ("flags", ctypes.c_uint32), ("num_waves", ctypes.c_int32),
+        ("min_range_pages", ctypes.c_int32), ("prof_events", ctypes.c_void_p),
     ]
 
 
@@ -181,8 +180,8 @@ def _kv_geometry(k_pages, v_pages, num_kv_heads, page_size, head_dim, kv_dtype):
 
 def make_decode_desc(*, num_seqs, num_q_heads, num_kv_heads, head_dim, page_size,
                      block_table_stride, num_pages, kv_dtype=DORA_KV_BF16, sm_scale=0.0,
-                     k_scales=None, v_scales=None, page_owner=None, flags=0, split_pages=0,
-                     target_units=0, prof_events=None) -> dora_decode_desc:
+                     k_scales=None, v_scales=None, page_owner=None, flags=0, num_waves=0,
+                     min_range_pages=0, prof_events=None) -> dora_decode_desc:
     d = dora_decode_desc()
     d.num_seqs, d.num_q_heads, d.num_kv_heads = num_seqs, num_q_heads, num_kv_heads
     d.head_dim, d.page_size, d.block_table_stride = head_dim, page_size, block_table_stride
@@ -190,7 +189,7 @@ def make_decode_desc(*, num_seqs, num_q_heads, num_kv_heads, head_dim, page_size
     d.k_scales = None if k_scales is None else k_scales.data_ptr()
     d.v_scales = None if v_scales is None else v_scales.data_ptr()
     d.page_owner = None if page_owner is None else page_owner.data_ptr()
-    d.flags, d.split_pages, d.target_units = flags, split_pages, target_units
+    d.flags, d.num_waves, d.min_range_pages = flags, num_waves, min_range_pages
     d.prof_events = prof_events
     return d
 
@@ -205,15 +204,17 @@ _ws_cache = {}
 def dora_decode_attn(q, k_pages, v_pages, block_table, seq_lens, version_ids, out, *,
                      num_kv_heads: int, page_size: int, kv_dtype: int = DORA_KV_BF16,
                      sm_scale: float = 0.0, k_scales=None, v_scales=None, page_owner=None,
-                     flags: int = 0, split_pages: int = 0, target_units: int = 0,
+                     flags: int = 0, num_waves: int = 0, min_range_pages: int = 0,
                      workspace=None, stream=None, prof_events=None):
     """Decode-step attention over the paged pool (see include/dora.h).
 
     q, out: bf16 [B][Hq][d]; k_pages: [num_pages][Hkv][d/X][P][X]; v_pages:
     [num_pages][Hkv][d][P] (bf16, or uint8 / float8_e4m3fn codes with fp32
     k_scales / v_scales [num_pages]); block_table int32 [B][stride]; seq_lens,
-    version_ids int32 [B].  The workspace is allocated (and cached per device
-    and size) when not given.  Returns `out`.
+    version_ids int32 [B].  num_waves / min_range_pages override how the
+    work is cut (0 = library default).  prof_events: 3 raw hipEvent_t handles.
+    The workspace is allocated (and cached per device and size) when not
+    given.  Returns `out`.
     """
     torch = _torch()
     B, Hq, D = (int(x) for x in q.shape)
@@ -222,7 +223,9 @@ def dora_decode_attn(q, k_pages, v_pages, block_table, seq_lens, version_ids, ou
         raise ValueError("block_table must be [B][stride]")
     stride = int(block_table.shape[1])
     if prof_events is not None:
-        arr = (ctypes.c_void_p * 4)(*[ctypes.c_void_p(e) for e in prof_events])
+        if len(prof_events) != 3:
+            raise ValueError("prof_events needs 3 event handles")
+        arr = (ctypes.c_void_p * 3)(*[ctypes.c_void_p(e) for e in prof_events])
         ev_ptr = ctypes.cast(arr, ctypes.c_void_p)
     else:
         arr, ev_ptr = None, None
@@ -230,8 +233,8 @@ def dora_decode_attn(q, k_pages, v_pages, block_table, seq_lens, version_ids, ou
                             page_size=page_size, block_table_stride=max(1, stride),
                             num_pages=num_pages, kv_dtype=kv_dtype, sm_scale=sm_scale,
                             k_scales=k_scales, v_scales=v_scales, page_owner=page_owner,
-                            flags=flags, split_pages=split_pages, target_units=target_units,
-                            prof_events=ev_ptr)
+                            flags=flags, num_waves=num_waves,
+                            min_range_pages=min_range_pages, prof_events=ev_ptr)
     if B == 0:
         return out
     args = [

@@ -60,8 +60,12 @@ def test_workspace_bytes(d):
     assert d.dora_decode_workspace_bytes(_desc(d, page_size=8)) == 0
     assert d.dora_decode_workspace_bytes(_desc(d, num_q_heads=7)) == 0       # not a multiple
     assert d.dora_decode_workspace_bytes(_desc(d, kv_dtype=5)) == 0
-    forced = _desc(d, flags=d.DORA_FLAG_FORCE_SPLIT, split_pages=1)
-    assert d.dora_decode_workspace_bytes(forced) >= 4 * 64 * 16
+    # two partial slots per decode wavefront
+    few = d.dora_decode_workspace_bytes(_desc(d, num_waves=10))
+    many = d.dora_decode_workspace_bytes(_desc(d, num_waves=1000))
+    assert many - few >= 990 * 2 * 4 * 128 * 4
+    assert d.dora_decode_workspace_bytes(_desc(d, num_kv_heads=128, num_q_heads=128)) == 0
+    assert d.dora_decode_workspace_bytes(_desc(d, block_table_stride=1 << 19)) == 0
 
 
 FAKE = 0x10000  # aligned non-null stand-in; never dereferenced (calls fail validation)
@@ -81,7 +85,8 @@ def test_decode_host_validation(d):
     assert _call(d, _desc(d, head_dim=96)) == d.DORA_ERR_UNSUPPORTED
     assert _call(d, _desc(d, num_q_heads=34, num_kv_heads=2)) == d.DORA_ERR_UNSUPPORTED
     assert _call(d, _desc(d, flags=0x80)) == d.DORA_ERR_INVALID_ARG
-    assert _call(d, _desc(d, flags=d.DORA_FLAG_FORCE_SPLIT)) == d.DORA_ERR_INVALID_ARG
+    assert _call(d, _desc(d, num_waves=-1)) == d.DORA_ERR_INVALID_ARG
+    assert _call(d, _desc(d, min_range_pages=-2)) == d.DORA_ERR_INVALID_ARG
     assert _call(d, _desc(d, sm_scale=-1.0)) == d.DORA_ERR_INVALID_ARG
     assert _call(d, _desc(d), q=0) == d.DORA_ERR_INVALID_ARG
     assert _call(d, _desc(d), ws=0) == d.DORA_ERR_INVALID_ARG

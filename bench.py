@@ -184,19 +184,25 @@ def time_pack(torch, dora, b, steps, flush):
 
 
 def copy_bandwidth(torch, nbytes=2 << 30):
+    """Measured reference rates: a device copy (read + write) and a read-only
+    reduction, both over 2 GiB."""
     a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1)
     c = torch.empty_like(a)
-    for _ in range(3):
-        c.copy_(a)
-    s, e = make_events(torch, 2)
-    s.record()
-    for _ in range(10):
-        c.copy_(a)
-    e.record()
-    torch.cuda.synchronize()
-    ms = s.elapsed_time(e) / 10
+    r = torch.empty((), dtype=torch.float32, device="cuda")
+    out = {}
+    for name, fn, moved in (("copy_gbps_measured", lambda: c.copy_(a), 2 * nbytes),
+                            ("read_gbps_measured", lambda: torch.sum(a, dim=0, out=r), nbytes)):
+        for _ in range(3):
+            fn()
+        s, e = make_events(torch, 2)
+        s.record()
+        for _ in range(10):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        out[name] = moved / (s.elapsed_time(e) / 10 * 1e-3) / 1e9
     del a, c
-    return 2 * nbytes / (ms * 1e-3) / 1e9
+    return out
 
 
 def cpu_baseline(b, budget_s=20.0):
@@ -318,7 +324,7 @@ def main():
             del b
         torch.cuda.empty_cache()
 
-    copy_gbps = copy_bandwidth(torch)
+    ref_rates = copy_bandwidth(torch)
     w = main_batch.w
     ab = main_rec["algorithmic_bytes"]["total"]
     split_s = main_rec["split_kernel_ms"] * 1e-3
@@ -348,7 +354,7 @@ def main():
         "hbm_gbps": main_rec["hbm_gbps"],
         "hbm_frac_of_peak": main_rec["hbm_frac_of_peak"],
         "context_tokens_per_s": main_rec["context_tokens_per_s"],
-        "copy_gbps_measured": copy_gbps,
+        **ref_rates,
         "roofline": {
             "bound": "hbm",
             "kernel": "decode_kernel",

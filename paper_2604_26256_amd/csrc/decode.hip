@@ -127,17 +127,26 @@ __device__ __forceinline__ bf16x4 fp8x4_to_bf16(uint32_t w0) {
   return bf16x4{a[0], a[1], b[0], b[1]};
 }
 
+// K: lane reads token tile_token(t, col) of 16-byte chunk (4s + grp); the chunk
+// and sub-tile strides are compile-time constants, so every K load is the
+// lane's base offset plus an immediate.  V: 16 head-dim rows per load, rows
+// 16 * P elements apart.  Every KV byte is read once per call, so the loads
+// are non-temporal (no cache allocation for streaming data).
 template <int D, int P, bool FP8>
 __device__ __forceinline__ void load_page(PageRegs<D, P, FP8>& r, const uint8_t* kbase,
-                                          const uint8_t* vbase, const uint32_t* koff,
-                                          uint32_t voff) {
+                                          const uint8_t* vbase, uint32_t koff, uint32_t voff) {
   typedef PageRegs<D, P, FP8> R;
+  constexpr int per_t = R::NK / R::NT;
 #pragma unroll
-  for (int i = 0; i < R::NK; ++i) r.k[i] = *(const u32x4*)(kbase + koff[i]);
+  for (int t = 0; t < R::NT; ++t)
+#pragma unroll
+    for (int s = 0; s < per_t; ++s)
+      r.k[t * per_t + s] =
+          __builtin_nontemporal_load((const u32x4*)(kbase + koff + (4 * s * P + 4 * t) * 16));
   constexpr int vrow = P * (FP8 ? 1 : 2) * 16;  // bytes between 16-row blocks of V
 #pragma unroll
   for (int i = 0; i < D / 16; ++i)
-    r.v[i] = *(const typename R::vraw_t*)(vbase + voff + i * vrow);
+    r.v[i] = __builtin_nontemporal_load((const typename R::vraw_t*)(vbase + voff + i * vrow));
 }
 
 // Page-head descriptor word: j (19 bits) | g << 19 (7 bits) | last << 26 |
@@ -148,7 +157,7 @@ __device__ __forceinline__ bool desc_last(uint32_t d) { return (d >> 26) & 1u; }
 __device__ __forceinline__ int desc_nvalid(uint32_t d) { return (int)(d >> 27) + 1; }
 
 template <int D, int P, bool FP8, int NBUF>
-__global__ __launch_bounds__(64) void decode_kernel(DecodeParams p) {
+__global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   typedef PageRegs<D, P, FP8> R;
   constexpr int NT = R::NT;
   constexpr int KSTEPS = D / 32;
@@ -220,15 +229,8 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeParams p) {
     }
   };
 
-  // Per-lane byte offsets inside a (page, KV head) tile.
-  uint32_t koff[R::NK];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    const int tok = tile_token<P>(t, col);
-    constexpr int per_t = R::NK / NT;
-#pragma unroll
-    for (int s = 0; s < per_t; ++s) koff[t * per_t + s] = ((4 * s + grp) * P + tok) * 16;
-  }
+  // Per-lane byte offsets inside a (page, KV head) tile (sub-tile 0, k-step 0).
+  const uint32_t koff = (uint32_t)((grp * P + tile_token<P>(0, col)) * 16);
   const uint32_t voff = (uint32_t)((col * P + (P == 16 ? 4 : 8) * grp) * E);
   const int64_t pb = p.page_bytes;
 

@@ -164,6 +164,8 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   constexpr int DBLK = D / 16;
   constexpr int E = FP8 ? 1 : 2;
   constexpr int TILE_BYTES = P * D * E;  // one KV head of one page
+  // next-segment query prefetch, where the register budget allows it
+  constexpr bool QPF = !(P == 32 && !FP8 && D == 128);
   extern __shared__ int sN[];            // page prefix over sequences, [B + 1]
 
   const int lane = threadIdx.x;
@@ -241,7 +243,22 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   int seg_b = 0, seg_g = 0;
   bool seg_whole = false, first_seg = true;
 
-  auto start_segment = [&](int b, int g, bool whole) {
+  // Query operand of (b, g): lane supplies q[head col][8 head-dim values] per
+  // k-step, in the head-dim order the K chunks are consumed in.
+  auto load_q = [&](bf16x8(&dst)[KSTEPS], int b, int g) {
+    const uint16_t* qrow = p.q + ((int64_t)b * Hq + (int64_t)g * G + col) * D;
+#pragma unroll
+    for (int s = 0; s < KSTEPS; ++s) {
+      const int d0 = FP8 ? 64 * (s >> 1) + 16 * grp + 8 * (s & 1) : 32 * s + 8 * grp;
+      dst[s] = col < G ? *(const bf16x8*)(qrow + d0) : bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+  };
+  // The query of the next segment is fetched together with that segment's
+  // first page (q_next, tagged with the page-head where the segment starts).
+  bf16x8 q_next[QPF ? KSTEPS : 1];
+  int64_t q_next_at = -1;
+
+  auto start_segment = [&](int b, int g, bool whole, int64_t x) {
     seg_b = b;
     seg_g = g;
     seg_whole = whole;
@@ -249,12 +266,12 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
     l_run = 0.f;
 #pragma unroll
     for (int i = 0; i < DBLK; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // Query operand: lane supplies q[head col][8 head-dim values] per k-step.
-    const uint16_t* qrow = p.q + ((int64_t)b * Hq + (int64_t)g * G + col) * D;
+    if (x == x0) return;  // the range's first query was loaded up front
+    if (QPF && q_next_at == x) {
 #pragma unroll
-    for (int s = 0; s < KSTEPS; ++s) {
-      const int dst = FP8 ? 64 * (s >> 1) + 16 * grp + 8 * (s & 1) : 32 * s + 8 * grp;
-      qop[s] = col < G ? *(const bf16x8*)(qrow + dst) : bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      for (int s = 0; s < (QPF ? KSTEPS : 1); ++s) qop[s] = q_next[s];
+    } else {
+      load_q(qop, b, g);  // a second segment start inside the prefetch window
     }
   };
 
@@ -400,6 +417,12 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
     const uint32_t info = (uint32_t)__builtin_amdgcn_readlane((int)cb_info, i);
     s_b[r] = b;
     s_info[r] = info;
+    if constexpr (QPF) {
+      if (desc_j(info) == 0 && x > x0 && x > q_next_at) {
+        load_q(q_next, b, desc_g(info));
+        q_next_at = x;
+      }
+    }
     const int64_t tile = (int64_t)pid * pb + (int64_t)desc_g(info) * TILE_BYTES;
     if constexpr (FP8) {
       s_ks[r] = p.k_scales[pid] * p.scale_log2;
@@ -411,6 +434,8 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
     load_page<D, P, FP8>(buf[r], p.k_pages + tile, p.v_pages + tile, koff, voff);
   };
 
+  load_q(qop, __builtin_amdgcn_readlane(cb_b, 0),
+         desc_g((uint32_t)__builtin_amdgcn_readlane((int)cb_info, 0)));
 #pragma unroll
   for (int k = 0; k < NBUF - 1; ++k) prefetch(k, x0 + k);
   int64_t x = x0;
@@ -420,7 +445,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
       prefetch((r + NBUF - 1) % NBUF, x + NBUF - 1);
       const uint32_t info = s_info[r];
       const int j = desc_j(info);
-      if (x == x0 || j == 0) start_segment(s_b[r], desc_g(info), j == 0);
+      if (x == x0 || j == 0) start_segment(s_b[r], desc_g(info), j == 0, x);
       consume(buf[r], desc_nvalid(info), s_ks[r], s_vs[r]);
       if (desc_last(info) || x == x1 - 1) {
         seg_whole = seg_whole && desc_last(info);
@@ -438,22 +463,12 @@ done:;
 
 constexpr int kCombineThreads = 1024;
 
-// Merge (M, S) with (m, l): S is a sum of 2^(x - M) terms.
-__device__ __forceinline__ void lse_merge(float& M, float& S, float m, float l) {
-  if (m > M) {
-    S = S * __builtin_amdgcn_exp2f(M - m) + l;
-    M = m;
-  } else if (m > -__builtin_inff()) {
-    S += l * __builtin_amdgcn_exp2f(m - M);
-  }
-}
-
-// One workgroup per (sequence, KV head).  Pass 1: the per-head max and
-// normaliser over the partials (one online pass, merged in LDS).  Pass 2: the
-// weighted sum of the partial outputs by (head, 4 head-dim values) tasks x
-// partial groups, the groups summed in LDS.  The k-th wavefront holding part
-// of the segment is wa + k; wa's partial is in slot 2wa + 1 unless its range
-// starts exactly at the segment (then slot 2wa), every later one's in 2w.
+// One workgroup per (sequence, KV head).  Threads are (head, 4 head-dim
+// values) tasks x partial groups; each thread folds its partials into a
+// running (max, normaliser, weighted sum) with one pass of loads, and the
+// groups are merged in LDS.  The k-th wavefront holding part of the segment is
+// wa + k; wa's partial is in slot 2wa + 1 unless its range starts exactly at
+// the segment (then slot 2wa), every later one's in 2w.
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(CombineParams p) {
   __shared__ float sM[kCombineThreads], sS[kCombineThreads];
   __shared__ f32x4 sAcc[kCombineThreads];
@@ -463,65 +478,65 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(CombineParams 
   const int t = threadIdx.x;
   const int G = p.group, D = p.head_dim;
   const int Nb = p.prefix[b], nb = p.prefix[b + 1] - Nb;
+  const int total = p.prefix[p.num_seqs];
   if (nb == 0) {  // empty sequence: zero output
     for (int e = t; e < G * D; e += kCombineThreads)
       p.out[((int64_t)b * p.num_q_heads + g * G) * D + e] = 0;
     return;
   }
-  const int64_t T = (int64_t)Hkv * p.prefix[p.num_seqs];
+  const int64_t T = (int64_t)Hkv * total;
   const int64_t W = effective_waves(T, p.launched_waves, p.min_range);
   const int64_t s0 = (int64_t)Hkv * Nb + (int64_t)g * nb;
   const int64_t wa = wave_of(s0, T, W), wb = wave_of(s0 + nb - 1, T, W);
   if (wa == wb) return;  // finished in place by the decode kernel
   const int np = (int)(wb - wa + 1);
   const int first_off = range_begin(wa, T, W) == s0 ? 0 : 1;
-  auto slot_of = [&](int k) -> int64_t { return 2 * (wa + k) + (k == 0 ? first_off : 0); };
 
-  {
-    const int n = t & 15, sl = t >> 4;
-    float M = -__builtin_inff(), S = 0.f;
-    if (n < G)
-      for (int k = sl; k < np; k += kCombineThreads / 16) {
-        const float2 ml = p.part_ml[slot_of(k) * G + n];
-        lse_merge(M, S, ml.x, ml.y);
-      }
-    sM[t] = M;
-    sS[t] = S;
-  }
-  __syncthreads();
-  for (int off = kCombineThreads / 2; off >= 16; off >>= 1) {
-    if (t < off) {
-      float M = sM[t], S = sS[t];
-      lse_merge(M, S, sM[t + off], sS[t + off]);
-      sM[t] = M;
-      sS[t] = S;
-    }
-    __syncthreads();
-  }
   const int tasks = G * (D / 4);
   const int tasks_r = (tasks + 63) & ~63;
   const int groups = kCombineThreads / tasks_r;  // >= 2 since tasks <= 512
   const int task = t % tasks_r, sg = t / tasks_r;
+  const bool active = task < tasks && sg < groups;
+  const int n = active ? task / (D / 4) : 0, d4 = active ? task - n * (D / 4) : 0;
+  float M = -__builtin_inff(), S = 0.f;
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (task < tasks && sg < groups) {
-    const int n = task / (D / 4), d4 = task - n * (D / 4);
-    const float M = sM[n];
+  if (active) {
     for (int k = sg; k < np; k += groups) {
-      const int64_t row = slot_of(k) * G + n;
-      const float wgt = __builtin_amdgcn_exp2f(p.part_ml[row].x - M);
+      const int64_t row = (2 * (wa + k) + (k == 0 ? first_off : 0)) * G + n;
+      const float2 ml = p.part_ml[row];
       const f32x4 o = *(const f32x4*)(p.part_o + row * D + 4 * d4);
-      acc += wgt * o;
+      if (ml.x > M) {
+        const float sc = __builtin_amdgcn_exp2f(M - ml.x);
+        acc = acc * sc + o;
+        S = S * sc + ml.y;
+        M = ml.x;
+      } else {
+        const float wgt = __builtin_amdgcn_exp2f(ml.x - M);
+        acc += wgt * o;
+        S += wgt * ml.y;
+      }
     }
   }
+  sM[t] = M;
+  sS[t] = S;
   sAcc[t] = acc;
   __syncthreads();
   if (sg == 0 && task < tasks) {
-    for (int k = 1; k < groups; ++k) acc += sAcc[k * tasks_r + task];
-    const int n = task / (D / 4), d4 = task - n * (D / 4);
-    const float inv = 1.f / sS[n];
+    float Mx = M;
+    for (int k = 1; k < groups; ++k) Mx = fmaxf(Mx, sM[k * tasks_r + task]);
+    f32x4 num = f32x4{0.f, 0.f, 0.f, 0.f};
+    float den = 0.f;
+    for (int k = 0; k < groups; ++k) {
+      const int i = k * tasks_r + task;
+      if (sM[i] == -__builtin_inff()) continue;  // a group with no partials
+      const float sc = __builtin_amdgcn_exp2f(sM[i] - Mx);
+      num += sc * sAcc[i];
+      den += sc * sS[i];
+    }
+    const float inv = 1.f / den;
     uint16_t* o = p.out + ((int64_t)b * p.num_q_heads + g * G + n) * D + 4 * d4;
-    *(bf16x4*)o = bf16x4{(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv),
-                         (__bf16)(acc[2] * inv), (__bf16)(acc[3] * inv)};
+    *(bf16x4*)o = bf16x4{(__bf16)(num[0] * inv), (__bf16)(num[1] * inv),
+                         (__bf16)(num[2] * inv), (__bf16)(num[3] * inv)};
   }
 }
 

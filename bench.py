@@ -35,7 +35,17 @@ import workloads as wl  # noqa: E402
 METRIC = "decode-attn tokens/s and HBM GB/s (% of peak) on long-tail length mixes"
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 MAIN_WORKLOAD = "rollout7b"
-PROFILE_PMC = os.path.join(ROOT, "profiles", "split_decode_rollout7b_pmc.json")
+PROFILES = os.path.join(ROOT, "profiles")
+PROFILE_PMC = os.path.join(PROFILES, "decode_kernel_rollout7b_pmc.json")
+DECODE_KERNEL = "dora::decode_kernel"
+CALIBRATION_KERNEL = "__amd_rocclr_copyBuffer"   # the 2 GiB device copy in copy_bandwidth()
+CALIBRATION_BYTES = 2 << 30                        # read and written per dispatch
+TRACE_CMD = ("cd /tmp && rocprofv3 --kernel-trace --stats --output-format csv "
+             "-d $REPO/gpurun_out/prof_trace -o run -- python $REPO/bench.py --only-main "
+             "--no-cpu-baseline --steps 30")
+PMC_CMD = ("cd /tmp && timeout -s KILL 300 rocprofv3 --pmc {c} --output-format csv "
+           "-d $REPO/gpurun_out/pmc_{c} -o run -- python $REPO/bench.py --only-main "
+           "--no-cpu-baseline --steps 5 --warmup 1")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2604_26256_amd", "csrc", f)
                   for f in ("decode.hip", "dora_internal.h", "api.cpp")]
 
@@ -65,7 +75,98 @@ def parse():
                     help="evict caches by reading (clean lines) or writing 1 GiB")
     ap.add_argument("--num-waves", type=int, default=0,
                     help="decode wavefronts (0 = one per resident slot)")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="write the kernel-trace summary of a rocprofv3 run under profiles/")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write the HBM-traffic summary of two rocprofv3 --pmc runs")
     return ap.parse_args()
+
+
+# ---------------------------------------------------------------------------
+# rocprofv3 summaries (CPU only: they read the CSV files a GPU run wrote)
+# ---------------------------------------------------------------------------
+
+def _find_csv(d, suffix):
+    for root, _, files in os.walk(d):
+        for f in files:
+            if f.endswith(suffix):
+                return os.path.join(root, f)
+    raise FileNotFoundError(f"no *{suffix} under {d}")
+
+
+def summarize_trace(d, workload):
+    import csv
+    rows = list(csv.DictReader(open(_find_csv(d, "kernel_stats.csv"))))
+    out = os.path.join(PROFILES, f"decode_kernel_{workload}_trace.md")
+    lines = [f"# rocprofv3 kernel trace: {workload} (main bench workload)", "",
+             "Command (repo root as $REPO):", "", "    " + TRACE_CMD, "",
+             "Per-kernel durations from `run_kernel_stats.csv` (all dispatches of the run:",
+             "warm-up, timed steps and the per-kernel event pass).", "",
+             "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
+    for r in rows:
+        name = r.get("Name") or r.get("KernelName") or ""
+        if not any(k in name for k in ("dora::", "reduce_kernel", CALIBRATION_KERNEL)):
+            continue
+        avg = float(r.get("AverageNs") or r.get("AvgNs")) / 1e3
+        lines.append(f"| `{name[:70]}` | {r['Calls']} | {avg:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    lines += ["", f"Kernel source hash: `{kernel_source_hash()}`", ""]
+    os.makedirs(PROFILES, exist_ok=True)
+    open(out, "w").write("\n".join(lines))
+    print(out)
+
+
+def summarize_pmc(fetch_dir, write_dir, workload):
+    import csv
+
+    def per_kernel(d, counter):
+        acc = {}
+        for r in csv.DictReader(open(_find_csv(d, "counter_collection.csv"))):
+            if r["Counter_Name"] != counter:
+                continue
+            acc.setdefault(r["Kernel_Name"], []).append((int(r["Grid_Size"]),
+                                                         float(r["Counter_Value"])))
+        return acc
+
+    fetch = per_kernel(fetch_dir, "FETCH_SIZE")
+    write = per_kernel(write_dir, "WRITE_SIZE")
+
+    def pick(acc, key, largest_grid=False):
+        vals = [v for k, lst in acc.items() if key in k for v in lst]
+        if not vals:
+            raise ValueError(f"no dispatches of {key} in the counter data")
+        if largest_grid:
+            g = max(v[0] for v in vals)
+            vals = [v for v in vals if v[0] == g]
+        return sum(v[1] for v in vals) / len(vals), len(vals)
+
+    cf, ncf = pick(fetch, CALIBRATION_KERNEL, largest_grid=True)
+    cw, ncw = pick(write, CALIBRATION_KERNEL, largest_grid=True)
+    ff = CALIBRATION_BYTES / (cf * 1024)
+    fw = CALIBRATION_BYTES / (cw * 1024)
+    df, ndf = pick(fetch, DECODE_KERNEL)
+    dw, ndw = pick(write, DECODE_KERNEL)
+    w = wl.BY_NAME[workload]
+    lengths = wl.sample_lengths(w, wl.seeds(wl.WORKLOADS.index(w))[0])
+    ab = wl.algorithmic_bytes(w, lengths)["total"]
+    traffic = df * 1024 * ff + dw * 1024 * fw
+    summary = {
+        "workload": workload, "kernel": "decode_kernel",
+        "kernel_source_hash": kernel_source_hash(),
+        "commands": [PMC_CMD.format(c="FETCH_SIZE"), PMC_CMD.format(c="WRITE_SIZE")],
+        "fetch_kib_per_dispatch": df, "write_kib_per_dispatch": dw,
+        "dispatches": {"fetch": ndf, "write": ndw},
+        "calibration": {"kernel": CALIBRATION_KERNEL, "bytes_read_and_written": CALIBRATION_BYTES,
+                        "fetch_kib": cf, "write_kib": cw, "dispatches": [ncf, ncw],
+                        "fetch_factor": ff, "write_factor": fw},
+        "traffic_bytes_per_launch": traffic,
+        "algorithmic_bytes_per_launch": ab,
+        "traffic_over_algorithmic": traffic / ab,
+    }
+    os.makedirs(PROFILES, exist_ok=True)
+    out = os.path.join(PROFILES, f"decode_kernel_{workload}_pmc.json")
+    json.dump(summary, open(out, "w"), indent=1)
+    print(out)
 
 
 def make_events(torch, n):
@@ -269,6 +370,12 @@ def load_pmc_traffic(w, lengths):
 
 def main():
     args = parse()
+    if args.summarize_trace or args.summarize_pmc:
+        if args.summarize_trace:
+            summarize_trace(args.summarize_trace, args.workload)
+        if args.summarize_pmc:
+            summarize_pmc(*args.summarize_pmc, args.workload)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(the decode path shards by sequence with no exchange; see DESIGN.md)",

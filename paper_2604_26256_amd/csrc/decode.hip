@@ -389,8 +389,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
 
   // 3. stream the range.  Descriptors come in chunks of 64 (current and next);
   // NBUF page buffers rotate so that NBUF-1 pages are in flight while one is
-  // consumed.  Past the end the last page-head is re-requested (a cache hit),
-  // so every iteration issues the same loads.
+  // consumed; every iteration issues the same loads.
   int cb_b, cb_pid, nb_b, nb_pid;
   uint32_t cb_info, nb_info;
   describe(x0, cb_b, cb_pid, cb_info);
@@ -403,7 +402,11 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   float s_ks[NBUF], s_vs[NBUF];
 
   auto prefetch = [&](int r, int64_t x) {
-    if (x >= x1) x = x1 - 1;
+    // Past the end of the range the loads still issue (uniform load count per
+    // iteration) but every lane reads the same address of the last tile, so
+    // each load is a single cache-line request.
+    const bool past = x >= x1;
+    if (past) x = x1 - 1;
     if (x - chunk >= 64) {
       chunk += 64;
       cb_b = nb_b;
@@ -431,7 +434,8 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
       s_ks[r] = p.scale_log2;
       s_vs[r] = 1.f;
     }
-    load_page<D, P, FP8>(buf[r], p.k_pages + tile, p.v_pages + tile, koff, voff);
+    load_page<D, P, FP8>(buf[r], p.k_pages + tile, p.v_pages + tile, past ? 0u : koff,
+                         past ? 0u : voff);
   };
 
   load_q(qop, __builtin_amdgcn_readlane(cb_b, 0),

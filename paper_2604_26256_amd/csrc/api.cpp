@@ -66,13 +66,12 @@ int64_t decode_waves(const dora_decode_desc& d) {
 }
 
 bool ws_layout(const dora_decode_desc& d, int64_t waves, WsLayout* out) {
-  const int64_t B = d.num_seqs < kMaxSeqsPerLaunch ? d.num_seqs : kMaxSeqsPerLaunch;
   const int64_t G = d.num_q_heads / d.num_kv_heads;
   WsLayout w;
   w.waves = waves;
   size_t off = kWsHeaderBytes;
-  w.prefix_off = off;
-  off = align_up(off + (size_t)(B + 1) * 4);
+  w.cuts_off = off;
+  off = align_up(off + (size_t)waves * 16);
   w.part_o_off = off;
   off = align_up(off + (size_t)(2 * waves) * G * d.head_dim * 4);
   w.part_ml_off = off;
@@ -162,7 +161,7 @@ dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const 
     dp.block_table = block_table + (int64_t)c0 * d.block_table_stride;
     dp.seq_lens = seq_lens + c0;
     dp.out = (uint16_t*)out + c0 * qrow;
-    dp.prefix = (int32_t*)(ws + w.prefix_off);
+    dp.cuts = (int4*)(ws + w.cuts_off);
     dp.part_o = (float*)(ws + w.part_o_off);
     dp.part_ml = (float2*)(ws + w.part_ml_off);
     dp.num_seqs = nb;
@@ -176,9 +175,8 @@ dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const 
     if (launch_decode(dp, d.head_dim, d.page_size, fp8, w.waves, s) != hipSuccess)
       return DORA_ERR_HIP;
     if (ev && c0 == 0 && hipEventRecord(ev[1], s) != hipSuccess) return DORA_ERR_HIP;
-    CombineParams cp{dp.prefix, dp.part_o, dp.part_ml, dp.out, nb, d.num_q_heads,
-                     d.num_kv_heads, G, d.head_dim, dp.min_range, w.waves};
-    if (launch_combine(cp, s) != hipSuccess) return DORA_ERR_HIP;
+    CombineParams cp{dp.cuts, dp.part_o, dp.part_ml, dp.out, d.num_q_heads, G, d.head_dim};
+    if (launch_combine(cp, w.waves, s) != hipSuccess) return DORA_ERR_HIP;
   }
   if (ev && hipEventRecord(ev[2], s) != hipSuccess) return DORA_ERR_HIP;
   return DORA_OK;

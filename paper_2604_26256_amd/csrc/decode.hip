@@ -31,9 +31,11 @@
 //            groups use cross-lane shuffles.  fp8 (OCP E4M3FN) pages are
 //            converted to bf16 in registers (exact) and the per-page scales are
 //            folded into the scores (K) and the probabilities (V).
-//   combine  one workgroup per (b, g): zero output for an empty sequence, and
-//            for a segment that spans several ranges the log-sum-exp merge of
-//            their partial results.
+//            Each wavefront records the one cut segment whose first piece it
+//            holds (at most one: its last segment), and writes the zero output
+//            of a share of the empty sequences.
+//   combine  one workgroup per wavefront: the log-sum-exp merge of the pieces
+//            of the cut segment that wavefront recorded.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -195,14 +197,21 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   }
   if (lane == 0) sN[B] = carry;
   __syncthreads();
-  if (blockIdx.x == 0)  // the combine kernel reads the prefix back
-    for (int b = lane; b <= B; b += 64) p.prefix[b] = sN[b];
+  const int64_t w = blockIdx.x;
+  // empty sequences: zero output, shared out over the launched wavefronts
+  for (int b = (int)w; b < B; b += gridDim.x) {
+    if (sN[b + 1] != sN[b]) continue;
+    uint32_t* o = (uint32_t*)(p.out + (int64_t)b * Hq * D);
+    for (int e = lane; e < Hq * D / 2; e += 64) o[e] = 0u;
+  }
 
   // 2. this wavefront's range of page-heads
   const int64_t T = (int64_t)Hkv * carry;
   const int64_t W = effective_waves(T, gridDim.x, p.min_range);
-  const int64_t w = blockIdx.x;
-  if (T == 0 || w >= W) return;
+  if (T == 0 || w >= W) {
+    if (lane == 0) p.cuts[w] = make_int4(-1, 0, 0, 0);
+    return;
+  }
   const int64_t x0 = range_begin(w, T, W), x1 = range_begin(w + 1, T, W);
 
   // Descriptors of 64 consecutive page-heads, one per lane: sequence, page id,
@@ -241,7 +250,8 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   bf16x8 qop[KSTEPS];
   float m_run = -__builtin_inff(), l_run = 0.f;
   int seg_b = 0, seg_g = 0;
-  bool seg_whole = false, first_seg = true;
+  bool seg_whole = false, seg_here = false, first_seg = true;
+  int4 cut = make_int4(-1, 0, 0, 0);  // the cut segment whose first piece is here
 
   // Query operand of (b, g): lane supplies q[head col][8 head-dim values] per
   // k-step, in the head-dim order the K chunks are consumed in.
@@ -262,6 +272,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
     seg_b = b;
     seg_g = g;
     seg_whole = whole;
+    seg_here = whole;  // the segment's first page is in this range
     m_run = -__builtin_inff();
     l_run = 0.f;
 #pragma unroll
@@ -295,6 +306,13 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
         for (int i = 0; i < DBLK; ++i) *(f32x4*)(po + 16 * i) = acc[i];
         if (grp == 0) p.part_ml[slot * G + col] = make_float2(m_run, l_tot);
       }
+    }
+    if (!seg_whole && seg_here) {
+      // pieces of this segment: ranges w .. wave_of(last page-head)
+      const int nb = sN[seg_b + 1] - sN[seg_b];
+      const int64_t s0 = (int64_t)Hkv * sN[seg_b] + (int64_t)seg_g * nb;
+      const int np = (int)(wave_of(s0 + nb - 1, T, W) - w + 1);
+      cut = make_int4(seg_b, seg_g, np, first_seg ? 0 : 1);
     }
     first_seg = false;
   };
@@ -458,7 +476,8 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
       if (++x >= x1) goto done;
     }
   }
-done:;
+done:
+  if (lane == 0) p.cuts[w] = cut;
 }
 
 // ---------------------------------------------------------------------------
@@ -466,36 +485,22 @@ done:;
 // ---------------------------------------------------------------------------
 
 constexpr int kCombineThreads = 1024;
+constexpr int kCombineBatch = 4;  // pieces whose loads a thread issues together
 
-// One workgroup per (sequence, KV head).  Threads are (head, 4 head-dim
-// values) tasks x partial groups; each thread folds its partials into a
-// running (max, normaliser, weighted sum) with one pass of loads, and the
-// groups are merged in LDS.  The k-th wavefront holding part of the segment is
-// wa + k; wa's partial is in slot 2wa + 1 unless its range starts exactly at
-// the segment (then slot 2wa), every later one's in 2w.
+// One workgroup per decode wavefront w.  If w recorded a cut segment, its np
+// pieces sit in the slots of wavefronts w .. w+np-1: w's in 2w + first_off,
+// every later one's in 2w'.  Threads are (head, 4 head-dim values) tasks x
+// piece groups; each folds its pieces into a running (max, normaliser,
+// weighted sum) with one pass of loads, and the groups are merged in LDS.
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(CombineParams p) {
   __shared__ float sM[kCombineThreads], sS[kCombineThreads];
   __shared__ f32x4 sAcc[kCombineThreads];
-  const int Hkv = p.num_kv_heads;
-  const int b = blockIdx.x / Hkv;
-  const int g = blockIdx.x - b * Hkv;
+  const int4 cut = p.cuts[blockIdx.x];
+  if (cut.x < 0) return;
+  const int64_t wa = blockIdx.x;
+  const int b = cut.x, g = cut.y, np = cut.z, first_off = cut.w;
   const int t = threadIdx.x;
   const int G = p.group, D = p.head_dim;
-  const int Nb = p.prefix[b], nb = p.prefix[b + 1] - Nb;
-  const int total = p.prefix[p.num_seqs];
-  if (nb == 0) {  // empty sequence: zero output
-    for (int e = t; e < G * D; e += kCombineThreads)
-      p.out[((int64_t)b * p.num_q_heads + g * G) * D + e] = 0;
-    return;
-  }
-  const int64_t T = (int64_t)Hkv * total;
-  const int64_t W = effective_waves(T, p.launched_waves, p.min_range);
-  const int64_t s0 = (int64_t)Hkv * Nb + (int64_t)g * nb;
-  const int64_t wa = wave_of(s0, T, W), wb = wave_of(s0 + nb - 1, T, W);
-  if (wa == wb) return;  // finished in place by the decode kernel
-  const int np = (int)(wb - wa + 1);
-  const int first_off = range_begin(wa, T, W) == s0 ? 0 : 1;
-
   const int tasks = G * (D / 4);
   const int tasks_r = (tasks + 63) & ~63;
   const int groups = kCombineThreads / tasks_r;  // >= 2 since tasks <= 512
@@ -505,19 +510,32 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(CombineParams 
   float M = -__builtin_inff(), S = 0.f;
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
   if (active) {
-    for (int k = sg; k < np; k += groups) {
-      const int64_t row = (2 * (wa + k) + (k == 0 ? first_off : 0)) * G + n;
-      const float2 ml = p.part_ml[row];
-      const f32x4 o = *(const f32x4*)(p.part_o + row * D + 4 * d4);
-      if (ml.x > M) {
-        const float sc = __builtin_amdgcn_exp2f(M - ml.x);
-        acc = acc * sc + o;
-        S = S * sc + ml.y;
-        M = ml.x;
-      } else {
-        const float wgt = __builtin_amdgcn_exp2f(ml.x - M);
-        acc += wgt * o;
-        S += wgt * ml.y;
+    for (int k0 = sg; k0 < np; k0 += groups * kCombineBatch) {
+      float2 ml[kCombineBatch];
+      f32x4 o[kCombineBatch];
+#pragma unroll
+      for (int i = 0; i < kCombineBatch; ++i) {  // all loads of the batch first
+        const int k = k0 + i * groups;
+        ml[i] = make_float2(-__builtin_inff(), 0.f);
+        o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (k < np) {
+          const int64_t row = (2 * (wa + k) + (k == 0 ? first_off : 0)) * G + n;
+          ml[i] = p.part_ml[row];
+          o[i] = *(const f32x4*)(p.part_o + row * D + 4 * d4);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kCombineBatch; ++i) {
+        if (ml[i].x > M) {
+          const float sc = __builtin_amdgcn_exp2f(M - ml[i].x);
+          acc = acc * sc + o[i];
+          S = S * sc + ml[i].y;
+          M = ml[i].x;
+        } else if (ml[i].x > -__builtin_inff()) {
+          const float wgt = __builtin_amdgcn_exp2f(ml[i].x - M);
+          acc += wgt * o[i];
+          S += wgt * ml[i].y;
+        }
       }
     }
   }
@@ -532,7 +550,7 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(CombineParams 
     float den = 0.f;
     for (int k = 0; k < groups; ++k) {
       const int i = k * tasks_r + task;
-      if (sM[i] == -__builtin_inff()) continue;  // a group with no partials
+      if (sM[i] == -__builtin_inff()) continue;  // a group with no pieces
       const float sc = __builtin_amdgcn_exp2f(sM[i] - Mx);
       num += sc * sAcc[i];
       den += sc * sS[i];
@@ -613,10 +631,9 @@ hipError_t launch_decode(const DecodeParams& p, int head_dim, int page_size, boo
                          dim3(64), args, decode_lds_bytes(p.num_seqs), s);
 }
 
-hipError_t launch_combine(const CombineParams& p, hipStream_t s) {
-  const int64_t grid = (int64_t)p.num_seqs * p.num_kv_heads;
-  if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL(combine_kernel, dim3((unsigned)grid), dim3(kCombineThreads), 0, s, p);
+hipError_t launch_combine(const CombineParams& p, int64_t waves, hipStream_t s) {
+  if (waves <= 0) return hipSuccess;
+  hipLaunchKernelGGL(combine_kernel, dim3((unsigned)waves), dim3(kCombineThreads), 0, s, p);
   return hipGetLastError();
 }
 

@@ -25,7 +25,7 @@ constexpr size_t kWsHeaderBytes = 256;
 // Workspace carve-up for one geometry (offsets in bytes from the base).
 struct WsLayout {
   int64_t waves;       // decode wavefronts launched (2 partial slots each)
-  size_t prefix_off;   // int32 [min(B, kMaxSeqsPerLaunch) + 1] page prefix
+  size_t cuts_off;     // int4 [waves] cut segment owned by each wavefront
   size_t part_o_off;   // float [2 * waves][G][D] unnormalised partial outputs
   size_t part_ml_off;  // float2 [2 * waves][G] {running max (log2 units), sum}
   size_t total;
@@ -46,7 +46,7 @@ struct DecodeParams {
   const int32_t* block_table;
   const int32_t* seq_lens;
   uint16_t* out;
-  int32_t* prefix;     // written by wavefront 0: page prefix [B + 1]
+  int4* cuts;          // per wavefront: {b, g, pieces, first-slot offset} or b = -1
   float* part_o;
   float2* part_ml;
   int32_t num_seqs, num_q_heads, num_kv_heads, group, stride;
@@ -56,13 +56,11 @@ struct DecodeParams {
 };
 
 struct CombineParams {
-  const int32_t* prefix;
+  const int4* cuts;
   const float* part_o;
   const float2* part_ml;
   uint16_t* out;
-  int32_t num_seqs, num_q_heads, num_kv_heads, group, head_dim;
-  int32_t min_range;
-  int64_t launched_waves;
+  int32_t num_q_heads, group, head_dim;
 };
 
 struct ValidateParams {
@@ -79,7 +77,7 @@ size_t decode_lds_bytes(int num_seqs);
 hipError_t decode_waves_per_cu(int head_dim, int page_size, bool fp8, int num_seqs, int* out);
 hipError_t launch_decode(const DecodeParams& p, int head_dim, int page_size, bool fp8,
                          int64_t waves, hipStream_t s);
-hipError_t launch_combine(const CombineParams& p, hipStream_t s);
+hipError_t launch_combine(const CombineParams& p, int64_t waves, hipStream_t s);
 hipError_t launch_validate(const ValidateParams& p, hipStream_t s);
 hipError_t launch_fill_i32(int32_t* dst, int32_t value, int64_t n, hipStream_t s);
 

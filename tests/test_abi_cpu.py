@@ -54,7 +54,8 @@ def _desc(d, **kw):
 def test_workspace_bytes(d):
     ok = d.dora_decode_workspace_bytes(_desc(d))
     assert ok > 0 and ok % 256 == 0
-    assert d.dora_decode_workspace_bytes(_desc(d, num_seqs=400)) > ok
+    # the workspace scales with the decode wavefronts, not with the batch
+    assert d.dora_decode_workspace_bytes(_desc(d, num_seqs=400)) == ok
     assert d.dora_decode_workspace_bytes(_desc(d, num_q_heads=36, num_kv_heads=2)) == 0  # G=18
     assert d.dora_decode_workspace_bytes(_desc(d, head_dim=96)) == 0
     assert d.dora_decode_workspace_bytes(_desc(d, page_size=8)) == 0

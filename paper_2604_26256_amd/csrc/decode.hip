@@ -72,24 +72,28 @@ __device__ __forceinline__ int wave_inclusive_scan(int v) {
   return v;
 }
 
-// Work range of wavefront w: [range_begin(w), range_begin(w + 1)).
-__device__ __forceinline__ int64_t range_begin(int64_t w, int64_t T, int64_t W) {
-  return w * T / W;
-}
+// A wave-uniform value, kept in a scalar register.
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // Number of wavefronts that take part: at most the launched count, and few
 // enough that every range holds at least min_range (>= 1) page-heads, so no
 // range is empty (W <= T).
-__device__ __forceinline__ int64_t effective_waves(int64_t T, int64_t launched,
-                                                   int64_t min_range) {
-  const int64_t want = (T + min_range - 1) / min_range;
+__device__ __forceinline__ int effective_waves(int T, int launched, int min_range) {
+  const int want = (T + min_range - 1) / min_range;
   return want < launched ? (want > 0 ? want : 1) : launched;
 }
 
-// Wavefront whose range holds page-head x: the largest w with begin(w) <= x.
-__device__ __forceinline__ int64_t wave_of(int64_t x, int64_t T, int64_t W) {
-  return ((x + 1) * W - 1) / T;
-}
+// Equal split of T page-heads into W ranges: with q = T / W and rem = T % W,
+// ranges 0 .. rem-1 hold q + 1 page-heads and the others q (q >= 1).
+struct Split {
+  int q, rem;
+  __device__ int begin(int w) const { return w * q + (w < rem ? w : rem); }
+  // the range that holds page-head x
+  __device__ int range_of(int x) const {
+    const int big = rem * (q + 1);
+    return x < big ? x / (q + 1) : rem + (x - big) / q;
+  }
+};
 
 // ---------------------------------------------------------------------------
 // decode
@@ -206,18 +210,21 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   }
 
   // 2. this wavefront's range of page-heads
-  const int64_t T = (int64_t)Hkv * carry;
-  const int64_t W = effective_waves(T, gridDim.x, p.min_range);
+  const int T = uni(Hkv * carry);  // fits in 32 bits: the host bounds batch x stride x Hkv
+  const int W = uni(effective_waves(T, (int)gridDim.x, p.min_range));
   if (T == 0 || w >= W) {
     if (lane == 0) p.cuts[w] = make_int4(-1, 0, 0, 0);
     return;
   }
-  const int64_t x0 = range_begin(w, T, W), x1 = range_begin(w + 1, T, W);
+  Split split;
+  split.q = uni(T / W);
+  split.rem = T - split.q * W;
+  const int x0 = split.begin((int)w), x1 = split.begin((int)w + 1);
 
   // Descriptors of 64 consecutive page-heads, one per lane: sequence, page id,
   // packed (j, g, last, valid tokens).
-  auto describe = [&](int64_t cbase, int& db, int& dpid, uint32_t& dinfo) {
-    const int64_t x = cbase + lane;
+  auto describe = [&](int cbase, int& db, int& dpid, uint32_t& dinfo) {
+    const int x = cbase + lane;
     db = 0;
     dpid = 0;
     dinfo = 0;
@@ -225,10 +232,10 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
       int lo = 0, hi = B;  // largest b with Hkv * N(b) <= x
       while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
-        if ((int64_t)Hkv * sN[mid] <= x) lo = mid; else hi = mid;
+        if (Hkv * sN[mid] <= x) lo = mid; else hi = mid;
       }
       const int nb = sN[lo + 1] - sN[lo];
-      const int r = (int)(x - (int64_t)Hkv * sN[lo]);
+      const int r = x - Hkv * sN[lo];
       const int g = r / nb;
       const int j = r - g * nb;
       int nv = p.seq_lens[lo] - j * P;
@@ -266,9 +273,9 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   // The query of the next segment is fetched together with that segment's
   // first page (q_next, tagged with the page-head where the segment starts).
   bf16x8 q_next[QPF ? KSTEPS : 1];
-  int64_t q_next_at = -1;
+  int q_next_at = -1;
 
-  auto start_segment = [&](int b, int g, bool whole, int64_t x) {
+  auto start_segment = [&](int b, int g, bool whole, int x) {
     seg_b = b;
     seg_g = g;
     seg_whole = whole;
@@ -308,10 +315,10 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
       }
     }
     if (!seg_whole && seg_here) {
-      // pieces of this segment: ranges w .. wave_of(last page-head)
+      // pieces of this segment: ranges w .. the range of its last page-head
       const int nb = sN[seg_b + 1] - sN[seg_b];
-      const int64_t s0 = (int64_t)Hkv * sN[seg_b] + (int64_t)seg_g * nb;
-      const int np = (int)(wave_of(s0 + nb - 1, T, W) - w + 1);
+      const int s0 = Hkv * sN[seg_b] + seg_g * nb;
+      const int np = split.range_of(s0 + nb - 1) - (int)w + 1;
       cut = make_int4(seg_b, seg_g, np, first_seg ? 0 : 1);
     }
     first_seg = false;
@@ -412,14 +419,14 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   uint32_t cb_info, nb_info;
   describe(x0, cb_b, cb_pid, cb_info);
   describe(x0 + 64, nb_b, nb_pid, nb_info);
-  int64_t chunk = x0;  // first page-head of the current descriptor chunk
+  int chunk = x0;  // first page-head of the current descriptor chunk
 
   R buf[NBUF];
   int s_b[NBUF];
   uint32_t s_info[NBUF];
   float s_ks[NBUF], s_vs[NBUF];
 
-  auto prefetch = [&](int r, int64_t x) {
+  auto prefetch = [&](int r, int x) {
     // Past the end of the range the loads still issue (uniform load count per
     // iteration) but every lane reads the same address of the last tile, so
     // each load is a single cache-line request.
@@ -432,7 +439,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
       cb_info = nb_info;
       describe(chunk + 64, nb_b, nb_pid, nb_info);
     }
-    const int i = (int)(x - chunk);
+    const int i = x - chunk;
     const int b = __builtin_amdgcn_readlane(cb_b, i);
     const int pid = __builtin_amdgcn_readlane(cb_pid, i);
     const uint32_t info = (uint32_t)__builtin_amdgcn_readlane((int)cb_info, i);
@@ -460,7 +467,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
          desc_g((uint32_t)__builtin_amdgcn_readlane((int)cb_info, 0)));
 #pragma unroll
   for (int k = 0; k < NBUF - 1; ++k) prefetch(k, x0 + k);
-  int64_t x = x0;
+  int x = x0;
   while (true) {
 #pragma unroll
     for (int r = 0; r < NBUF; ++r) {

@@ -36,16 +36,16 @@ METRIC = "decode-attn tokens/s and HBM GB/s (% of peak) on long-tail length mixe
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 MAIN_WORKLOAD = "rollout7b"
 PROFILES = os.path.join(ROOT, "profiles")
-PROFILE_PMC = os.path.join(PROFILES, "decode_kernel_rollout7b_pmc.json")
 DECODE_KERNEL = "dora::decode_kernel"
 CALIBRATION_KERNEL = "__amd_rocclr_copyBuffer"   # the 2 GiB device copy in copy_bandwidth()
 CALIBRATION_BYTES = 2 << 30                        # read and written per dispatch
 TRACE_CMD = ("cd /tmp && rocprofv3 --kernel-trace --stats --output-format csv "
-             "-d $REPO/gpurun_out/prof_trace -o run -- python $REPO/bench.py --only-main "
-             "--no-cpu-baseline --steps 30")
+             "-d $REPO/gpurun_out/prof_trace_{w} -o run -- python $REPO/bench.py --only-main "
+             "--workload {w} --no-cpu-baseline --steps 30")
 PMC_CMD = ("cd /tmp && timeout -s KILL 300 rocprofv3 --pmc {c} --output-format csv "
-           "-d $REPO/gpurun_out/pmc_{c} -o run -- python $REPO/bench.py --only-main "
-           "--no-cpu-baseline --steps 5 --warmup 1")
+           "-d $REPO/gpurun_out/pmc_{d}_{w} -o run -- python $REPO/bench.py --only-main "
+           "--workload {w} --no-cpu-baseline --steps 5 --warmup 1")
+L2_COUNTERS = "TCC_HIT_sum TCC_MISS_sum"
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2604_26256_amd", "csrc", f)
                   for f in ("decode.hip", "dora_internal.h", "api.cpp")]
 
@@ -77,8 +77,9 @@ def parse():
                     help="decode wavefronts (0 = one per resident slot)")
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="write the kernel-trace summary of a rocprofv3 run under profiles/")
-    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
-                    help="write the HBM-traffic summary of two rocprofv3 --pmc runs")
+    ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "L2_DIR"),
+                    help="write the HBM-traffic and L2 hit-rate summary of three "
+                         "rocprofv3 --pmc runs")
     return ap.parse_args()
 
 
@@ -94,12 +95,16 @@ def _find_csv(d, suffix):
     raise FileNotFoundError(f"no *{suffix} under {d}")
 
 
+def pmc_path(workload):
+    return os.path.join(PROFILES, f"decode_kernel_{workload}_pmc.json")
+
+
 def summarize_trace(d, workload):
     import csv
     rows = list(csv.DictReader(open(_find_csv(d, "kernel_stats.csv"))))
     out = os.path.join(PROFILES, f"decode_kernel_{workload}_trace.md")
-    lines = [f"# rocprofv3 kernel trace: {workload} (main bench workload)", "",
-             "Command (repo root as $REPO):", "", "    " + TRACE_CMD, "",
+    lines = [f"# rocprofv3 kernel trace: {workload}", "",
+             "Command (repo root as $REPO):", "", "    " + TRACE_CMD.format(w=workload), "",
              "Per-kernel durations from `run_kernel_stats.csv` (all dispatches of the run:",
              "warm-up, timed steps and the per-kernel event pass).", "",
              "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
@@ -116,7 +121,7 @@ def summarize_trace(d, workload):
     print(out)
 
 
-def summarize_pmc(fetch_dir, write_dir, workload):
+def summarize_pmc(fetch_dir, write_dir, l2_dir, workload):
     import csv
 
     def per_kernel(d, counter):
@@ -130,6 +135,8 @@ def summarize_pmc(fetch_dir, write_dir, workload):
 
     fetch = per_kernel(fetch_dir, "FETCH_SIZE")
     write = per_kernel(write_dir, "WRITE_SIZE")
+    hit = per_kernel(l2_dir, "TCC_HIT_sum")
+    miss = per_kernel(l2_dir, "TCC_MISS_sum")
 
     def pick(acc, key, largest_grid=False):
         vals = [v for k, lst in acc.items() if key in k for v in lst]
@@ -150,10 +157,16 @@ def summarize_pmc(fetch_dir, write_dir, workload):
     lengths = wl.sample_lengths(w, wl.seeds(wl.WORKLOADS.index(w))[0])
     ab = wl.algorithmic_bytes(w, lengths)["total"]
     traffic = df * 1024 * ff + dw * 1024 * fw
+    dh, _ = pick(hit, DECODE_KERNEL)
+    dm, _ = pick(miss, DECODE_KERNEL)
+    ch, _ = pick(hit, "dora::combine_kernel")
+    cm, _ = pick(miss, "dora::combine_kernel")
     summary = {
         "workload": workload, "kernel": "decode_kernel",
         "kernel_source_hash": kernel_source_hash(),
-        "commands": [PMC_CMD.format(c="FETCH_SIZE"), PMC_CMD.format(c="WRITE_SIZE")],
+        "commands": [PMC_CMD.format(c="FETCH_SIZE", d="FETCH_SIZE", w=workload),
+                     PMC_CMD.format(c="WRITE_SIZE", d="WRITE_SIZE", w=workload),
+                     PMC_CMD.format(c=f'"{L2_COUNTERS}"', d="L2", w=workload)],
         "fetch_kib_per_dispatch": df, "write_kib_per_dispatch": dw,
         "dispatches": {"fetch": ndf, "write": ndw},
         "calibration": {"kernel": CALIBRATION_KERNEL, "bytes_read_and_written": CALIBRATION_BYTES,
@@ -162,9 +175,13 @@ def summarize_pmc(fetch_dir, write_dir, workload):
         "traffic_bytes_per_launch": traffic,
         "algorithmic_bytes_per_launch": ab,
         "traffic_over_algorithmic": traffic / ab,
+        "l2": {"decode_kernel": {"hits_per_dispatch": dh, "misses_per_dispatch": dm,
+                                 "hit_rate": dh / (dh + dm)},
+               "combine_kernel": {"hits_per_dispatch": ch, "misses_per_dispatch": cm,
+                                  "hit_rate": ch / (ch + cm)}},
     }
     os.makedirs(PROFILES, exist_ok=True)
-    out = os.path.join(PROFILES, f"decode_kernel_{workload}_pmc.json")
+    out = pmc_path(workload)
     json.dump(summary, open(out, "w"), indent=1)
     print(out)
 
@@ -355,17 +372,17 @@ def _cpu_model():
     return "unknown"
 
 
-def load_pmc_traffic(w, lengths):
-    """HBM traffic of the split kernel from the committed rocprofv3 counter
-    summary, or None if absent or taken on a different kernel source."""
+def load_pmc(w):
+    """The committed rocprofv3 counter summary of this workload's decode
+    kernel, or None if absent or taken on a different kernel source."""
     try:
-        with open(PROFILE_PMC) as f:
+        with open(pmc_path(w.name)) as f:
             pmc = json.load(f)
     except (OSError, ValueError):
         return None
     if pmc.get("kernel_source_hash") != kernel_source_hash() or pmc.get("workload") != w.name:
         return None
-    return pmc.get("traffic_bytes_per_launch")
+    return pmc
 
 
 def main():
@@ -415,6 +432,9 @@ def main():
                         flush, args.num_waves)
         rec = decode_record(w, b.lengths, t)
         rec["kv_dtype"] = "bf16" if w.kv_dtype == 0 else "fp8_e4m3"
+        pmc = load_pmc(w)
+        rec["split_kernel_traffic_bytes"] = pmc["traffic_bytes_per_launch"] if pmc else None
+        rec["split_kernel_l2_hit_rate"] = pmc["l2"]["decode_kernel"]["hit_rate"] if pmc else None
         if w.pack_seqs:
             log(f"workload {name}: pack/unpack")
             rec["pack_unpack"] = time_pack(torch, dora, b, max(5, steps // 2), flush)
@@ -435,7 +455,7 @@ def main():
     w = main_batch.w
     ab = main_rec["algorithmic_bytes"]["total"]
     split_s = main_rec["split_kernel_ms"] * 1e-3
-    traffic = load_pmc_traffic(w, main_batch.lengths)
+    traffic = main_rec["split_kernel_traffic_bytes"]
     line = {
         "metric": METRIC,
         "value": main_rec["decode_tokens_per_s"],
@@ -470,6 +490,7 @@ def main():
             "unit": "GB/s",
             "frac": ab / split_s / 1e9 / HBM_PEAK_GBPS,
             "traffic": traffic,
+            "l2_hit_rate": main_rec["split_kernel_l2_hit_rate"],
             "algorithmic_bytes_per_launch": ab,
             "avg_launch_ms": main_rec["split_kernel_ms"],
         },

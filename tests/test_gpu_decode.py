@@ -209,3 +209,20 @@ def test_full_size_workloads_sampled(idx):
     assert err <= TOL[w.kv_dtype], err
     del b
     torch.cuda.empty_cache()
+
+
+def test_profiling_events_bracket_each_kernel():
+    """The three events bracket the decode and the combine kernel: positive
+    durations, and the call's result is unchanged."""
+    lens = np.array([3000, 17, 900, 4000, 1], np.int32)
+    w = _w(B=len(lens), Hq=28, Hkv=4, d=128, P=16, dt=0, lens=lens)
+    b = gpu_batch(w, lengths=lens, seed_index=15)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    for e in evs:
+        e.record()
+    torch.cuda.synchronize()
+    ref = run_decode(b).clone()
+    out = run_decode(b, prof_events=[e.cuda_event for e in evs])
+    assert torch.equal(out, ref)
+    dec, comb = (evs[i].elapsed_time(evs[i + 1]) for i in range(2))
+    assert 0 < dec < 1000 and 0 < comb < 1000, (dec, comb)

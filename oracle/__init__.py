@@ -36,7 +36,9 @@ def build(force: bool = True) -> str:
     """Compile dora_oracle.c into liboracle.so (gcc, OpenMP)."""
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp"
-        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"]
+        # -ffp-contract=off: the append's fp32 steps must round one by one
+        cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
+               _SRC, "-o", tmp, "-lm"]
         subprocess.run(cmd, check=True)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
@@ -67,6 +69,11 @@ def _load():
     lib.oracle_unpack.argtypes = [c_i, c_i, c_i, c_i, c_i64, c_i, c_p, c_p, c_i64, c_p, c_p,
                                   c_p, c_p]
     lib.oracle_unpack.restype = c_i
+    lib.oracle_f32_to_e4m3.argtypes = [ctypes.c_float]
+    lib.oracle_f32_to_e4m3.restype = ctypes.c_uint8
+    lib.oracle_kv_append.argtypes = [c_i, c_i, c_i, c_i, c_i64, c_i, c_i, c_p, c_p, c_p, c_p,
+                                     c_p, c_p, c_p, c_p]
+    lib.oracle_kv_append.restype = c_i
     lib.oracle_max_threads.argtypes = []
     lib.oracle_max_threads.restype = c_i
     _lib = lib
@@ -208,3 +215,38 @@ def unpack(packed, dst_pages, k_pages, v_pages, *, kv_dtype, page_size, num_kv_h
     return int(_load().oracle_unpack(kv_dtype, page_size, num_kv_heads, head_dim, num_pages,
                                      policy_version, _ptr(pk), _ptr(dst), int(dst.size),
                                      _ptr(kp), _ptr(vp), _ptr(k_scales), _ptr(v_scales)))
+
+
+def f32_to_e4m3(x) -> np.ndarray:
+    """Nearest OCP E4M3FN code of each fp32 value (ties to even, saturating)."""
+    f = _load().oracle_f32_to_e4m3
+    xs = np.asarray(x, dtype=np.float32).reshape(-1)
+    return np.array([f(float(v)) for v in xs], dtype=np.uint8).reshape(np.shape(x))
+
+
+def kv_append(k_new, v_new, block_table, seq_lens, k_pages, v_pages, *, kv_dtype, page_size,
+              k_scales=None, v_scales=None) -> int:
+    """Store each sequence's token seq_lens[b] - 1 (k_new / v_new: bf16 codes
+    [B][Hkv][d]) into its page slot, in place in the numpy page arrays (and, for
+    fp8, the per-page scales).  Returns the C status code."""
+    kn = np.ascontiguousarray(k_new)
+    vn = np.ascontiguousarray(v_new)
+    if kn.dtype != np.uint16:
+        kn = kn.view(np.uint16)
+    if vn.dtype != np.uint16:
+        vn = vn.view(np.uint16)
+    B, Hkv, d = kn.shape
+    for a in (k_pages, v_pages, k_scales, v_scales):
+        if a is not None and not a.flags.c_contiguous:
+            raise ValueError("pages and scales must be C-contiguous (written in place)")
+    kp = k_pages.view(np.uint8).reshape(-1)
+    vp = v_pages.view(np.uint8).reshape(-1)
+    pb = Hkv * page_size * d * (2 if kv_dtype == 0 else 1)
+    bt = _c(block_table, np.int32)
+    lens = _c(seq_lens, np.int32)
+    if kv_dtype == 1 and (k_scales is None or v_scales is None or
+                          k_scales.dtype != np.float32 or v_scales.dtype != np.float32):
+        raise ValueError("fp8 pages need float32 k_scales / v_scales arrays")
+    return int(_load().oracle_kv_append(B, Hkv, d, page_size, kp.size // pb, max(1, bt.shape[1]),
+                                        kv_dtype, _ptr(bt), _ptr(lens), _ptr(kn), _ptr(vn),
+                                        _ptr(kp), _ptr(vp), _ptr(k_scales), _ptr(v_scales)))

@@ -26,7 +26,8 @@
  *   fp8 pages carry one fp32 scale per page for K and one for V.
  *
  * Return codes: 0 ok, 1 invalid argument, 2 page id out of range,
- *               3 page not owned by the sequence's version.
+ *               3 page not owned by the sequence's version,
+ *               5 (append) sequence longer than its block-table row.
  */
 #include <math.h>
 #include <stdint.h>
@@ -362,6 +363,125 @@ int oracle_unpack(int kv_dtype, int P, int Hkv, int d, int64_t num_pages, int po
       k_scales[dst_pages[j]] = ks[j];
       v_scales[dst_pages[j]] = vs[j];
     }
+  }
+  return OR_OK;
+}
+
+/* ---------------------------------------------------------------------------
+ * KV append: the write that precedes every decode step.  Each sequence's
+ * current token (the one whose query the next decode step attends with, its
+ * K/V counted in seq_lens, Sec. 2.2) is stored into its page slot.
+ * ------------------------------------------------------------------------- */
+
+/* The E4M3FN code nearest to the fp32 value x on the format's grid, ties to
+ * the even mantissa, saturating to +-448 (the largest finite value) instead of
+ * overflowing.  The grid: in binade [2^e, 2^(e+1)), e >= -6, the spacing is
+ * 2^(e-3); below 2^-6 (subnormals and zero) it is 2^-9.  NaN gives the NaN
+ * code. */
+uint8_t oracle_f32_to_e4m3(float x) {
+  if (isnan(x)) return (uint8_t)(signbit(x) ? 0xFF : 0x7F);
+  const uint8_t sign = signbit(x) ? 0x80 : 0x00;
+  const double a = fabs((double)x);
+  if (a >= 448.0) return (uint8_t)(sign | 0x7E);
+  const double min_normal = ldexp(1.0, -6);
+  int e2;
+  frexp(a, &e2); /* a = f * 2^e2, f in [0.5, 1): a lies in binade e2 - 1 */
+  const double quantum = a < min_normal ? ldexp(1.0, -9) : ldexp(1.0, e2 - 1 - 3);
+  const double v = nearbyint(a / quantum) * quantum; /* exact scaling; ties to even */
+  if (v < min_normal) return (uint8_t)(sign | (uint8_t)(v / ldexp(1.0, -9)));
+  int ev2;
+  const double f = frexp(v, &ev2); /* v = f * 2^ev2: exponent ev2 - 1, mantissa 2f - 1 */
+  return (uint8_t)(sign | (((ev2 - 1 + 7) << 3) | (int)((2.0 * f - 1.0) * 8.0)));
+}
+
+static float e4m3_to_f32(uint8_t c) { return (float)oracle_e4m3_to_f64(c); }
+
+static float bf16_to_f32(uint16_t bits) { return (float)oracle_bf16_to_f64(bits); }
+
+/* Byte offset of element (head h, token slot t, dim i) inside one page. */
+static int64_t k_off(int kv_dtype, int d, int P, int h, int t, int i) {
+  const int X = kv_dtype == 0 ? 8 : 16;
+  return ((((int64_t)h * (d / X) + i / X) * P + t) * X + i % X) * (kv_dtype == 0 ? 2 : 1);
+}
+static int64_t v_off(int kv_dtype, int d, int P, int h, int t, int i) {
+  return (((int64_t)h * d + i) * P + t) * (kv_dtype == 0 ? 2 : 1);
+}
+
+/* Store one token's Hkv x d values x (bf16 bits) into page `page` at slot `slot`
+ * of one pool (K when is_k, else V).  fp8 page-scale policy, all in fp32:
+ *   amax = max |x|
+ *   slot 0:                       s = max(amax, 2^-126) / 448
+ *   slot > 0 and amax / s0 > 448: s = amax / 448, and each earlier code c of
+ *                                 the page (all heads) becomes
+ *                                 enc((dec(c) * s0) / s)
+ *   otherwise:                    s = s0   (s0 = the page's current scale)
+ *   the token's codes enc(x / s); the page's scale becomes s. */
+static void append_token(int kv_dtype, int Hkv, int d, int P, int is_k, int64_t page, int slot,
+                         const uint16_t* x, uint8_t* pages, float* scales) {
+  const int64_t pb = (int64_t)Hkv * P * d * (kv_dtype == 0 ? 2 : 1);
+  uint8_t* pg = pages + page * pb;
+  if (kv_dtype == 0) {
+    for (int h = 0; h < Hkv; ++h)
+      for (int i = 0; i < d; ++i) {
+        const int64_t off = is_k ? k_off(0, d, P, h, slot, i) : v_off(0, d, P, h, slot, i);
+        memcpy(pg + off, &x[(int64_t)h * d + i], 2);
+      }
+    return;
+  }
+  float amax = 0.0f;
+  for (int64_t e = 0; e < (int64_t)Hkv * d; ++e) {
+    const float a = fabsf(bf16_to_f32(x[e]));
+    if (a > amax) amax = a;
+  }
+  float s;
+  if (slot == 0) {
+    const float floor_ = ldexpf(1.0f, -126);
+    s = (amax > floor_ ? amax : floor_) / 448.0f;
+  } else {
+    const float s0 = scales[page];
+    if (amax / s0 > 448.0f) {
+      s = amax / 448.0f;
+      for (int t = 0; t < slot; ++t)
+        for (int h = 0; h < Hkv; ++h)
+          for (int i = 0; i < d; ++i) {
+            const int64_t off = is_k ? k_off(1, d, P, h, t, i) : v_off(1, d, P, h, t, i);
+            const float old = e4m3_to_f32(pg[off]) * s0;
+            pg[off] = oracle_f32_to_e4m3(old / s);
+          }
+    } else {
+      s = s0;
+    }
+  }
+  for (int h = 0; h < Hkv; ++h)
+    for (int i = 0; i < d; ++i) {
+      const int64_t off = is_k ? k_off(1, d, P, h, slot, i) : v_off(1, d, P, h, slot, i);
+      pg[off] = oracle_f32_to_e4m3(bf16_to_f32(x[(int64_t)h * d + i]) / s);
+    }
+  scales[page] = s;
+}
+
+/* For every sequence b with L = seq_lens[b] >= 1, token t = L - 1 (k_new[b],
+ * v_new[b]: bf16 [Hkv][d]) goes to page block_table[b][t / P], slot t % P.
+ * Sequences are processed in order.  Returns 1 on invalid arguments, 2 if a
+ * page id is out of range, 5 if L exceeds the block-table row (stride * P);
+ * nothing is written for a failing sequence. */
+int oracle_kv_append(int B, int Hkv, int d, int P, int64_t num_pages, int stride, int kv_dtype,
+                     const int32_t* block_table, const int32_t* seq_lens,
+                     const uint16_t* k_new, const uint16_t* v_new, uint8_t* k_pages,
+                     uint8_t* v_pages, float* k_scales, float* v_scales) {
+  if (B < 0 || Hkv < 1 || (d != 64 && d != 128) || (P != 16 && P != 32) || stride < 1 ||
+      (kv_dtype != 0 && kv_dtype != 1) || (kv_dtype == 1 && (!k_scales || !v_scales)))
+    return OR_BAD_ARG;
+  for (int b = 0; b < B; ++b) {
+    const int L = seq_lens[b];
+    if (L <= 0) continue;
+    if ((int64_t)L > (int64_t)stride * P) return 5;
+    const int t = L - 1;
+    const int64_t page = block_table[(int64_t)b * stride + t / P];
+    if (page < 0 || page >= num_pages) return OR_PAGE_RANGE;
+    const int64_t n = (int64_t)Hkv * d;
+    append_token(kv_dtype, Hkv, d, P, 1, page, t % P, k_new + b * n, k_pages, k_scales);
+    append_token(kv_dtype, Hkv, d, P, 0, page, t % P, v_new + b * n, v_pages, v_scales);
   }
   return OR_OK;
 }

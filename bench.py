@@ -257,6 +257,32 @@ def decode_record(w, lengths, t):
     }
 
 
+def time_append(torch, dora, b, steps, flush):
+    """KV append of one token per sequence (each sequence rewrites its last
+    token, so every page it writes exists), cache evicted before each call."""
+    w = b.w
+    g = torch.Generator(device="cuda").manual_seed(77)
+    kn = torch.randn(w.num_seqs, w.num_kv_heads, w.head_dim, generator=g, device="cuda").to(
+        torch.bfloat16)
+    vn = torch.randn(w.num_seqs, w.num_kv_heads, w.head_dim, generator=g, device="cuda").to(
+        torch.bfloat16)
+    kw = dict(num_kv_heads=w.num_kv_heads, page_size=w.page_size, kv_dtype=w.kv_dtype,
+              k_scales=b.k_scales, v_scales=b.v_scales)
+    ts = []
+    for i in range(steps + 2):
+        flush()
+        e0, e1 = make_events(torch, 2)
+        e0.record()
+        dora.dora_kv_append(kn, vn, b.block_table, b.seq_lens, b.k_pages, b.v_pages, **kw)
+        e1.record()
+        torch.cuda.synchronize()
+        if i >= 2:
+            ts.append(e0.elapsed_time(e1))
+    ab = wl.append_algorithmic_bytes(w, b.lengths)
+    ms = float(np.median(ts))
+    return {"ms": ms, "algorithmic_bytes": ab, "gbps": ab / (ms * 1e-3) / 1e9}
+
+
 def time_pack(torch, dora, b, steps, flush):
     """Pack + unpack of the 32-sequence same-version migration set."""
     w = b.w
@@ -435,6 +461,7 @@ def main():
         pmc = load_pmc(w)
         rec["split_kernel_traffic_bytes"] = pmc["traffic_bytes_per_launch"] if pmc else None
         rec["split_kernel_l2_hit_rate"] = pmc["l2"]["decode_kernel"]["hit_rate"] if pmc else None
+        rec["append"] = time_append(torch, dora, b, max(5, steps // 2), flush)
         if w.pack_seqs:
             log(f"workload {name}: pack/unpack")
             rec["pack_unpack"] = time_pack(torch, dora, b, max(5, steps // 2), flush)

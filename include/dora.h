@@ -158,6 +158,46 @@ dora_status dora_decode_attn(const dora_decode_desc* desc,
                              void* workspace, size_t workspace_bytes,
                              dora_stream_t stream);
 
+/* Store every sequence's current-token K and V into its page slot: the write
+ * that precedes each decode step (the per-token step of Sec. 2.2; seq_lens
+ * counts that token, so dora_decode_attn with the same seq_lens then attends
+ * over it).  Token t = seq_lens[b] - 1 of sequence b goes to page
+ * block_table[b][t / P], token slot t % P; seq_lens[b] = 0 appends nothing.
+ *   desc         the decode descriptor (num_seqs, num_kv_heads, head_dim,
+ *                page_size, block_table_stride, num_pages, kv_dtype; flags may
+ *                hold DORA_FLAG_VALIDATE; num_q_heads must be valid for it)
+ *   k_new, v_new device bf16 [B][Hkv][d], 16-byte aligned
+ *   block_table, seq_lens, version_ids  as for dora_decode_attn
+ *   k_pages, v_pages  device, the layouts above, written in place
+ *   k_scales, v_scales  device fp32 [num_pages], fp8 only (else ignored),
+ *                updated in place
+ *   dev_status   device int32 or NULL: receives DORA_OK, or
+ *                DORA_ERR_DEVICE_CHECK if some sequence was skipped because its
+ *                page id is out of range, its length exceeds its block-table
+ *                row, or (under DORA_FLAG_VALIDATE with desc->page_owner) its
+ *                page belongs to another version.  Skipped sequences write
+ *                nothing; no write ever leaves the pool.
+ * bf16 pages take the values as given.  fp8 pages: the paper fixes no
+ * quantisation policy; this library keeps one fp32 scale per page for K and one
+ * for V, grow-only, computed in fp32 with IEEE rounding:
+ *   amax = max |x| over the token's Hkv x d values
+ *   fresh = max(amax / 448, 2^-126)   (a normal fp32 number)
+ *   slot 0:                           s = fresh
+ *   slot > 0, not amax / s0 <= 448:   s = fresh, and every earlier code c of
+ *                                     the page (all heads) becomes
+ *                                     enc((dec(c) * s0) / s)
+ *   otherwise:                        s = s0       (s0: the page's scale)
+ *   codes of the token: enc(x / s); the page's scale becomes s.
+ * enc is the nearest OCP E4M3FN code, ties to even, saturating at +-448.
+ * The pages of one call must belong to distinct sequences (a page is never
+ * appended to by two sequences at once).  Enqueued on `stream`; one launch
+ * (two with dev_status). */
+dora_status dora_kv_append(const dora_decode_desc* desc, const void* k_new, const void* v_new,
+                           const int32_t* block_table, const int32_t* seq_lens,
+                           const int32_t* version_ids, void* k_pages, void* v_pages,
+                           float* k_scales, float* v_scales, int32_t* dev_status,
+                           dora_stream_t stream);
+
 /* ---------------------------------------------------------------------------
  * KV page pack / unpack: the device half of the paper's two-phase state
  * transfer for same-version migration (Sec. 3.4: request metadata travels by

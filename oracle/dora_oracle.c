@@ -409,13 +409,14 @@ static int64_t v_off(int kv_dtype, int d, int P, int h, int t, int i) {
 
 /* Store one token's Hkv x d values x (bf16 bits) into page `page` at slot `slot`
  * of one pool (K when is_k, else V).  fp8 page-scale policy, all in fp32:
- *   amax = max |x|
- *   slot 0:                       s = max(amax, 2^-126) / 448
- *   slot > 0 and amax / s0 > 448: s = amax / 448, and each earlier code c of
- *                                 the page (all heads) becomes
- *                                 enc((dec(c) * s0) / s)
- *   otherwise:                    s = s0   (s0 = the page's current scale)
- *   the token's codes enc(x / s); the page's scale becomes s. */
+ *   amax = max |x|;  fresh(a) = max(a / 448, 2^-126)  (a normal number)
+ *   slot 0:                            s = fresh(amax)
+ *   slot > 0 and not amax / s0 <= 448: s = fresh(amax), and each earlier code c
+ *                                      of the page (all heads) becomes
+ *                                      enc((dec(c) * s0) / s)
+ *   otherwise:                         s = s0  (s0 = the page's current scale)
+ *   the token's codes enc(x / s); the page's scale becomes s.
+ * ("not <=" also grows when amax / s0 is NaN, i.e. an unset zero scale.) */
 static void append_token(int kv_dtype, int Hkv, int d, int P, int is_k, int64_t page, int slot,
                          const uint16_t* x, uint8_t* pages, float* scales) {
   const int64_t pb = (int64_t)Hkv * P * d * (kv_dtype == 0 ? 2 : 1);
@@ -433,14 +434,15 @@ static void append_token(int kv_dtype, int Hkv, int d, int P, int is_k, int64_t 
     const float a = fabsf(bf16_to_f32(x[e]));
     if (a > amax) amax = a;
   }
+  const float min_normal = ldexpf(1.0f, -126);
+  const float fresh = amax / 448.0f > min_normal ? amax / 448.0f : min_normal;
   float s;
   if (slot == 0) {
-    const float floor_ = ldexpf(1.0f, -126);
-    s = (amax > floor_ ? amax : floor_) / 448.0f;
+    s = fresh;
   } else {
     const float s0 = scales[page];
-    if (amax / s0 > 448.0f) {
-      s = amax / 448.0f;
+    if (!(amax / s0 <= 448.0f)) {
+      s = fresh;
       for (int t = 0; t < slot; ++t)
         for (int h = 0; h < Hkv; ++h)
           for (int i = 0; i < d; ++i) {

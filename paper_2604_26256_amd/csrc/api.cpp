@@ -182,6 +182,44 @@ dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const 
   return DORA_OK;
 }
 
+dora_status dora_kv_append(const dora_decode_desc* desc, const void* k_new, const void* v_new,
+                           const int32_t* block_table, const int32_t* seq_lens,
+                           const int32_t* version_ids, void* k_pages, void* v_pages,
+                           float* k_scales, float* v_scales, int32_t* dev_status,
+                           dora_stream_t stream) {
+  dora_status st = check_desc(desc);
+  if (st != DORA_OK) return st;
+  const dora_decode_desc& d = *desc;
+  if (d.num_seqs == 0) return DORA_OK;
+  const bool fp8 = d.kv_dtype == DORA_KV_FP8_E4M3;
+  const bool validate = (d.flags & DORA_FLAG_VALIDATE) != 0;
+  if (!k_new || !v_new || !block_table || !seq_lens || !k_pages || !v_pages)
+    return DORA_ERR_INVALID_ARG;
+  if (fp8 && (!k_scales || !v_scales)) return DORA_ERR_INVALID_ARG;
+  if (validate && d.page_owner && !version_ids) return DORA_ERR_INVALID_ARG;
+  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_pages) || !aligned16(v_pages))
+    return DORA_ERR_INVALID_ARG;
+  AppendParams p;
+  p.k_new = (const uint16_t*)k_new;
+  p.v_new = (const uint16_t*)v_new;
+  p.block_table = block_table;
+  p.seq_lens = seq_lens;
+  p.version_ids = validate ? version_ids : nullptr;
+  p.page_owner = validate ? d.page_owner : nullptr;
+  p.k_pages = (uint8_t*)k_pages;
+  p.v_pages = (uint8_t*)v_pages;
+  p.k_scales = fp8 ? k_scales : nullptr;
+  p.v_scales = fp8 ? v_scales : nullptr;
+  p.dev_status = dev_status;
+  p.num_seqs = d.num_seqs;
+  p.num_kv_heads = d.num_kv_heads;
+  p.head_dim = d.head_dim;
+  p.page_size = d.page_size;
+  p.stride = d.block_table_stride;
+  p.num_pages = d.num_pages;
+  return launch_append(p, fp8, (hipStream_t)stream) == hipSuccess ? DORA_OK : DORA_ERR_HIP;
+}
+
 // ---------------------------------------------------------------------------
 // pack / unpack
 // ---------------------------------------------------------------------------

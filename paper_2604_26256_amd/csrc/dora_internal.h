@@ -79,6 +79,24 @@ hipError_t launch_decode(const DecodeParams& p, int head_dim, int page_size, boo
                          int64_t waves, hipStream_t s);
 hipError_t launch_combine(const CombineParams& p, int64_t waves, hipStream_t s);
 hipError_t launch_validate(const ValidateParams& p, hipStream_t s);
+
+struct AppendParams {
+  const uint16_t* k_new;       // bf16 [B][Hkv][d]
+  const uint16_t* v_new;
+  const int32_t* block_table;
+  const int32_t* seq_lens;
+  const int32_t* version_ids;  // ownership check when page_owner is set
+  const int16_t* page_owner;
+  uint8_t* k_pages;
+  uint8_t* v_pages;
+  float* k_scales;             // fp8 only
+  float* v_scales;
+  int32_t* dev_status;         // may be null
+  int32_t num_seqs, num_kv_heads, head_dim, page_size, stride;
+  int64_t num_pages;
+};
+
+hipError_t launch_append(const AppendParams& p, bool fp8, hipStream_t s);
 hipError_t launch_fill_i32(int32_t* dst, int32_t value, int64_t n, hipStream_t s);
 
 // 256-byte pack header, written by the pack kernel and checked by unpack.

@@ -75,6 +75,8 @@ _lib.dora_decode_workspace_bytes.argtypes = [_DescP]
 _lib.dora_decode_workspace_bytes.restype = _SZ
 _lib.dora_decode_attn.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
 _lib.dora_decode_attn.restype = ctypes.c_int
+_lib.dora_kv_append.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+_lib.dora_kv_append.restype = ctypes.c_int
 _lib.dora_kv_packed_bytes.argtypes = [_PackP, _I64]
 _lib.dora_kv_packed_bytes.restype = _SZ
 _lib.dora_kv_page_pack.argtypes = [_PackP, _P, _P, _P, _P, _P, _I64, _P, _SZ, _P]
@@ -269,6 +271,47 @@ def dora_decode_attn(q, k_pages, v_pages, block_table, seq_lens, version_ids, ou
     del arr
     _check(st, "dora_decode_attn")
     return out
+
+
+def dora_kv_append(k_new, v_new, block_table, seq_lens, k_pages, v_pages, *, num_kv_heads,
+                   page_size, kv_dtype=DORA_KV_BF16, k_scales=None, v_scales=None,
+                   version_ids=None, page_owner=None, flags=0, dev_status=None, stream=None):
+    """Store each sequence's current token (k_new / v_new: bf16 [B][Hkv][d],
+    token seq_lens[b] - 1) into its page slot, in place (see include/dora.h).
+    fp8 pools update their per-page k_scales / v_scales (fp32 [num_pages])."""
+    torch = _torch()
+    B, Hkv, D = (int(x) for x in k_new.shape)
+    if Hkv != num_kv_heads:
+        raise ValueError("k_new must be [B][num_kv_heads][head_dim]")
+    num_pages, kv_types = _kv_geometry(k_pages, v_pages, num_kv_heads, page_size, D, kv_dtype)
+    if block_table.dim() != 2 or block_table.shape[0] != B:
+        raise ValueError("block_table must be [B][stride]")
+    stride = int(block_table.shape[1])
+    desc = make_decode_desc(num_seqs=B, num_q_heads=num_kv_heads, num_kv_heads=num_kv_heads,
+                            head_dim=D, page_size=page_size, block_table_stride=max(1, stride),
+                            num_pages=num_pages, kv_dtype=kv_dtype, page_owner=page_owner,
+                            flags=flags)
+    if B == 0:
+        return
+    fp8 = kv_dtype == DORA_KV_FP8_E4M3
+    args = [
+        _dev_ptr(k_new, "k_new", (torch.bfloat16,), shape=(B, Hkv, D)),
+        _dev_ptr(v_new, "v_new", (torch.bfloat16,), shape=(B, Hkv, D)),
+        _dev_ptr(block_table, "block_table", (torch.int32,), shape=(B, stride), align=4),
+        _dev_ptr(seq_lens, "seq_lens", (torch.int32,), shape=(B,), align=4),
+        _opt_ptr(version_ids, "version_ids", (torch.int32,), shape=(B,), align=4),
+        _dev_ptr(k_pages, "k_pages", kv_types),
+        _dev_ptr(v_pages, "v_pages", kv_types),
+        _dev_ptr(k_scales, "k_scales", (torch.float32,), shape=(num_pages,), align=4)
+        if fp8 else None,
+        _dev_ptr(v_scales, "v_scales", (torch.float32,), shape=(num_pages,), align=4)
+        if fp8 else None,
+        _opt_ptr(dev_status, "dev_status", (torch.int32,), numel=1, align=4),
+    ]
+    if page_owner is not None:
+        _dev_ptr(page_owner, "page_owner", (torch.int16,), shape=(num_pages,), align=2)
+    _check(_lib.dora_kv_append(ctypes.byref(desc), *args, _stream_handle(stream)),
+           "dora_kv_append")
 
 
 # ---------------------------------------------------------------------------

@@ -100,6 +100,25 @@ def test_decode_host_validation(d):
                                         None) == d.DORA_ERR_INVALID_ARG
 
 
+def test_append_host_validation(d):
+    P = ctypes.c_void_p
+    lib = d.library()
+
+    def call(desc, kn=FAKE, vn=FAKE, bt=FAKE, lens=FAKE, kp=FAKE, vp=FAKE, ks=FAKE, vs=FAKE):
+        return lib.dora_kv_append(ctypes.byref(desc), P(kn), P(vn), P(bt), P(lens), None,
+                                  P(kp), P(vp), P(ks), P(vs), None, None)
+
+    assert call(_desc(d, head_dim=96)) == d.DORA_ERR_UNSUPPORTED
+    assert call(_desc(d, page_size=8)) == d.DORA_ERR_UNSUPPORTED
+    assert call(_desc(d, num_seqs=-1)) == d.DORA_ERR_INVALID_ARG
+    assert call(_desc(d), kn=0) == d.DORA_ERR_INVALID_ARG
+    assert call(_desc(d), kp=FAKE + 4) == d.DORA_ERR_INVALID_ARG              # misaligned
+    assert call(_desc(d, kv_dtype=1), ks=0) == d.DORA_ERR_INVALID_ARG          # fp8, no scales
+    assert call(_desc(d, num_seqs=0)) == d.DORA_OK                             # nothing to do
+    assert lib.dora_kv_append(None, None, None, None, None, None, None, None, None, None, None,
+                              None) == d.DORA_ERR_INVALID_ARG
+
+
 def test_pack_host_validation_and_size(d):
     lib = d.library()
     for dt in (0, 1):

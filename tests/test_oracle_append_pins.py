@@ -143,7 +143,7 @@ def test_append_fp8_first_token_of_a_page_is_torch_quantisation(P, Hkv, d):
     page = bt[0, 1]
     for new, pool, scales, slot_of in ((kn, k, ks, _k_slot), (vn, v, vs, _v_slot)):
         x = _bf16_f32(new[0])
-        s = np.float32(max(np.abs(x).max(), np.float32(2.0 ** -126))) / np.float32(448.0)
+        s = max(np.float32(np.abs(x).max()) / np.float32(448.0), np.float32(2.0 ** -126))
         assert scales[page] == s
         assert np.array_equal(slot_of(pool, page, 0), _torch_e4m3(x / s))
     others = [i for i in range(len(ks)) if i != page]

@@ -361,6 +361,17 @@ def subset_for_oracle(batch: Batch, seqs: Sequence[int]) -> dict:
     return out
 
 
+def append_algorithmic_bytes(w: Workload, lengths: np.ndarray) -> int:
+    """Bytes one KV append must move: the new token's bf16 K and V read, their
+    stored form written, its length and block-table entry, and for fp8 the two
+    page scales read and written.  Requantisation of a page whose scale grows
+    depends on the values and is not counted."""
+    active = int((np.asarray(lengths) > 0).sum())
+    n = w.num_kv_heads * w.head_dim
+    per = 2 * n * 2 + 2 * n * w.elem_bytes + 4 + 4 + (16 if w.kv_dtype == 1 else 0)
+    return active * per
+
+
 def algorithmic_bytes(w: Workload, lengths: np.ndarray) -> dict:
     """Bytes the decode step must move at least once: K and V of valid tokens,
     page scales (fp8), Q, the output, block-table entries and lengths."""

@@ -183,7 +183,7 @@ dora_status dora_decode_attn(const dora_decode_desc* desc,
  *   amax = max |x| over the token's Hkv x d values
  *   fresh = max(amax / 448, 2^-126)   (a normal fp32 number)
  *   slot 0:                           s = fresh
- *   slot > 0, not amax / s0 <= 448:   s = fresh, and every earlier code c of
+ *   slot > 0, not fresh <= s0:        s = fresh, and every earlier code c of
  *                                     the page (all heads) becomes
  *                                     enc((dec(c) * s0) / s)
  *   otherwise:                        s = s0       (s0: the page's scale)

@@ -409,14 +409,15 @@ static int64_t v_off(int kv_dtype, int d, int P, int h, int t, int i) {
 
 /* Store one token's Hkv x d values x (bf16 bits) into page `page` at slot `slot`
  * of one pool (K when is_k, else V).  fp8 page-scale policy, all in fp32:
- *   amax = max |x|;  fresh(a) = max(a / 448, 2^-126)  (a normal number)
- *   slot 0:                            s = fresh(amax)
- *   slot > 0 and not amax / s0 <= 448: s = fresh(amax), and each earlier code c
- *                                      of the page (all heads) becomes
- *                                      enc((dec(c) * s0) / s)
- *   otherwise:                         s = s0  (s0 = the page's current scale)
+ *   amax = max |x|;  fresh = max(amax / 448, 2^-126)  (a normal number)
+ *   slot 0:                        s = fresh
+ *   slot > 0 and not fresh <= s0:  s = fresh, and each earlier code c of the
+ *                                  page (all heads) becomes
+ *                                  enc((dec(c) * s0) / s)
+ *   otherwise:                     s = s0   (s0 = the page's current scale)
  *   the token's codes enc(x / s); the page's scale becomes s.
- * ("not <=" also grows when amax / s0 is NaN, i.e. an unset zero scale.) */
+ * The scales themselves are compared, so a token with the page's own maximum
+ * does not count as growth; "not <=" also grows an unset (NaN) scale. */
 static void append_token(int kv_dtype, int Hkv, int d, int P, int is_k, int64_t page, int slot,
                          const uint16_t* x, uint8_t* pages, float* scales) {
   const int64_t pb = (int64_t)Hkv * P * d * (kv_dtype == 0 ? 2 : 1);
@@ -441,7 +442,7 @@ static void append_token(int kv_dtype, int Hkv, int d, int P, int is_k, int64_t 
     s = fresh;
   } else {
     const float s0 = scales[page];
-    if (!(amax / s0 <= 448.0f)) {
+    if (!(fresh <= s0)) {
       s = fresh;
       for (int t = 0; t < slot; ++t)
         for (int h = 0; h < Hkv; ++h)

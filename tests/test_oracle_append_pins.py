@@ -230,3 +230,28 @@ def test_append_error_codes_and_empty_sequences():
     assert oracle.kv_append(kn, kn, bad, np.array([1], np.int32), k, v, **args) == 2
     for a, b in zip(before, (k, v, ks, vs)):
         assert np.array_equal(a, b)
+
+
+def test_append_fp8_token_with_the_page_maximum_does_not_grow_the_scale():
+    """Rewriting the last token with the values that set the page's scale (a
+    decode loop that retries a step) changes nothing, including where fp32
+    rounding puts amax / s0 just above 448."""
+    P, Hkv, d = 16, 8, 128
+    bt, (k, v, ks, vs) = _one_seq(P, Hkv, d)
+    g = torch.Generator().manual_seed(11)
+    toks = [torch.randn(Hkv, d, generator=g) * m for m in (0.1, 0.1, 0.05)]
+    # token 1's maximum is 0.51171875 (a bf16 value), for which
+    # 0.51171875 / (0.51171875 / 448) rounds above 448 in fp32
+    toks[1][0, 0] = 0.51171875
+    toks = [_bf16(x[None]) for x in toks]
+    for t, x in enumerate(toks):
+        assert oracle.kv_append(x, x, bt, np.array([t + 1], np.int32), k, v, kv_dtype=1,
+                                page_size=P, k_scales=ks, v_scales=vs) == 0
+    page = bt[0, 0]
+    snap = (k[page].copy(), v[page].copy(), ks[page], vs[page])
+    for _ in range(3):                              # token 1 set the scale; rewrite it
+        assert oracle.kv_append(toks[1], toks[1], bt, np.array([2], np.int32), k, v,
+                                kv_dtype=1, page_size=P, k_scales=ks, v_scales=vs) == 0
+    assert ks[page] == snap[2] and vs[page] == snap[3]
+    assert np.array_equal(_k_slot(k, page, 0), _k_slot(snap[0][None], 0, 0))
+    assert np.array_equal(k[page], snap[0]) and np.array_equal(v[page], snap[1])

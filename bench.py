@@ -321,10 +321,42 @@ def time_pack(torch, dora, b, steps, flush):
             pk.append(s0.elapsed_time(s1))
             up.append(s1b.elapsed_time(s2))
     moved = 2 * npg * w.page_bytes          # K and V pages, one way
-    return {"seqs": int(len(seqs)), "pages": int(npg), "bytes_one_way": int(moved),
-            "pack_ms": float(np.mean(pk)), "unpack_ms": float(np.mean(up)),
-            "pack_gbps_rw": 2 * moved / (np.mean(pk) * 1e-3) / 1e9,
-            "unpack_gbps_rw": 2 * moved / (np.mean(up) * 1e-3) / 1e9}
+    rec = {"seqs": int(len(seqs)), "pages": int(npg), "bytes_one_way": int(moved),
+           "pack_ms": float(np.mean(pk)), "unpack_ms": float(np.mean(up)),
+           "pack_gbps_rw": 2 * moved / (np.mean(pk) * 1e-3) / 1e9,
+           "unpack_gbps_rw": 2 * moved / (np.mean(up) * 1e-3) / 1e9}
+    rec["offload"] = time_offload(torch, dora, b, src_t, dst_t, packed, geo, len(seqs), moved,
+                                  max(3, steps // 2), flush)
+    return rec
+
+
+def time_offload(torch, dora, b, src_t, dst_t, packed, geo, n_seqs, moved, steps, flush):
+    """The same set packed straight into pinned host memory and unpacked from
+    it (offload and restore), beside plain device<->host copies of the packed
+    buffer, which bound what the host link carries."""
+    host = torch.empty(packed.numel(), dtype=torch.uint8, pin_memory=True)
+    runs = {"pack_to_host": lambda: dora.dora_kv_page_pack(
+                b.k_pages, b.v_pages, src_t, host, policy_version=0, n_seqs=n_seqs, **geo),
+            "unpack_from_host": lambda: dora.dora_kv_page_unpack(
+                host, dst_t, b.k_pages, b.v_pages, src_version=0, policy_version=0, **geo),
+            "d2h_copy": lambda: host.copy_(packed, non_blocking=True),
+            "h2d_copy": lambda: packed.copy_(host, non_blocking=True)}
+    out = {}
+    for name, fn in runs.items():
+        ts = []
+        for i in range(steps + 1):
+            flush()
+            e0, e1 = make_events(torch, 2)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            if i >= 1:
+                ts.append(e0.elapsed_time(e1))
+        ms = float(np.median(ts))
+        out[name + "_ms"] = ms
+        out[name + "_gbps"] = moved / (ms * 1e-3) / 1e9
+    return out
 
 
 def copy_bandwidth(torch, nbytes=2 << 30):

@@ -237,8 +237,13 @@ typedef struct {
 size_t dora_kv_packed_bytes(const dora_pack_desc* desc, int64_t n_pages);
 
 /* Gather pages src_pages[0..n_pages) (device int32, logical order) of a pool
- * into `packed` (device, >= dora_kv_packed_bytes bytes, 16-byte aligned) and
- * write the header.  k_scales/v_scales: device [num_pages], fp8 only. */
+ * into `packed` (>= dora_kv_packed_bytes bytes, 16-byte aligned) and write the
+ * header.  k_scales/v_scales: device [num_pages], fp8 only.
+ * `packed` may be device memory, or pinned host memory from hipHostMalloc
+ * (mapped: the kernel writes it over the host link).  The latter is the
+ * offload half of the paper's hierarchical memory management (Sec. 3.4: KV
+ * caches moved to host memory under VRAM pressure and restored for deferred
+ * generation); no device staging buffer is needed. */
 dora_status dora_kv_page_pack(const dora_pack_desc* desc,
                               const void* k_pages, const void* v_pages,
                               const float* k_scales, const float* v_scales,
@@ -253,7 +258,9 @@ dora_status dora_kv_page_pack(const dora_pack_desc* desc,
  * within one policy version).  On the device the header is checked against
  * desc and n_pages; on any mismatch nothing is written to the pool and, if
  * dev_status (device int32, may be NULL) is given, it receives a non-zero
- * dora_status code; it receives DORA_OK otherwise. */
+ * dora_status code; it receives DORA_OK otherwise.  `packed` may be device
+ * memory or pinned host memory from hipHostMalloc (restore from host: the
+ * kernel reads it over the host link). */
 dora_status dora_kv_page_unpack(const dora_pack_desc* desc, int32_t src_version,
                                 const void* packed, size_t packed_bytes,
                                 const int32_t* dst_pages, int64_t n_pages,

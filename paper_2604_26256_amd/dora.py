@@ -152,6 +152,20 @@ def _dev_ptr(t, name, dtypes, shape=None, numel=None, align=16):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _buf_ptr(t, name):
+    """A uint8 buffer the GPU can address: device memory, or pinned host memory
+    (torch's pin_memory allocations are hipHostMalloc'd and mapped, so the same
+    pointer works in kernels)."""
+    torch = _torch()
+    if isinstance(t, torch.Tensor) and t.device.type == "cpu":
+        if not t.is_pinned():
+            raise ValueError(f"{name}: host buffers must be pinned (pin_memory=True)")
+        if t.dtype != torch.uint8 or not t.is_contiguous() or t.data_ptr() % 16:
+            raise ValueError(f"{name}: contiguous, 16-byte aligned uint8 required")
+        return ctypes.c_void_p(t.data_ptr())
+    return _dev_ptr(t, name, (torch.uint8,))
+
+
 def _opt_ptr(t, name, dtypes, **kw):
     return None if t is None else _dev_ptr(t, name, dtypes, **kw)
 
@@ -334,7 +348,8 @@ def dora_kv_packed_bytes(desc: dora_pack_desc, n_pages: int) -> int:
 def dora_kv_page_pack(k_pages, v_pages, src_pages, packed, *, num_kv_heads, page_size, head_dim,
                       kv_dtype=DORA_KV_BF16, policy_version=0, n_seqs=1, k_scales=None,
                       v_scales=None, stream=None):
-    """Gather pages src_pages (device int32) into `packed` (device uint8)."""
+    """Gather pages src_pages (device int32) into `packed`: a device uint8
+    buffer, or a pinned host one (offload to host memory)."""
     torch = _torch()
     num_pages, kv_types = _kv_geometry(k_pages, v_pages, num_kv_heads, page_size, head_dim,
                                        kv_dtype)
@@ -351,7 +366,7 @@ def dora_kv_page_pack(k_pages, v_pages, src_pages, packed, *, num_kv_heads, page
         _dev_ptr(v_scales, "v_scales", (torch.float32,), shape=(num_pages,), align=4) if fp8
         else None,
         _dev_ptr(src_pages, "src_pages", (torch.int32,), numel=n, align=4) if n else None, n,
-        _dev_ptr(packed, "packed", (torch.uint8,)), packed.numel(), _stream_handle(stream))
+        _buf_ptr(packed, "packed"), packed.numel(), _stream_handle(stream))
     _check(st, "dora_kv_page_pack")
     return packed
 
@@ -359,8 +374,9 @@ def dora_kv_page_pack(k_pages, v_pages, src_pages, packed, *, num_kv_heads, page
 def dora_kv_page_unpack(packed, dst_pages, k_pages, v_pages, *, src_version, num_kv_heads,
                         page_size, head_dim, kv_dtype=DORA_KV_BF16, policy_version=0,
                         k_scales=None, v_scales=None, dev_status=None, stream=None):
-    """Scatter `packed` into pages dst_pages of a destination pool of version
-    policy_version; src_version is the version tag of the migrating request."""
+    """Scatter `packed` (device, or pinned host memory: restore from host) into
+    pages dst_pages of a destination pool of version policy_version;
+    src_version is the version tag of the migrating request."""
     torch = _torch()
     num_pages, kv_types = _kv_geometry(k_pages, v_pages, num_kv_heads, page_size, head_dim,
                                        kv_dtype)
@@ -370,7 +386,7 @@ def dora_kv_page_unpack(packed, dst_pages, k_pages, v_pages, *, src_version, num
     n = int(dst_pages.numel())
     fp8 = kv_dtype == DORA_KV_FP8_E4M3
     st = _lib.dora_kv_page_unpack(
-        ctypes.byref(desc), int(src_version), _dev_ptr(packed, "packed", (torch.uint8,)),
+        ctypes.byref(desc), int(src_version), _buf_ptr(packed, "packed"),
         packed.numel(),
         _dev_ptr(dst_pages, "dst_pages", (torch.int32,), numel=n, align=4) if n else None, n,
         _dev_ptr(k_pages, "k_pages", kv_types), _dev_ptr(v_pages, "v_pages", kv_types),

@@ -269,6 +269,33 @@ dora_status dora_kv_page_unpack(const dora_pack_desc* desc, int32_t src_version,
                                 int32_t* dev_status, dora_stream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * Orchestrator planners (host, integer arithmetic; Sec. 3.3).  Versions are
+ * indexed oldest first; the last index is the latest version.
+ * ------------------------------------------------------------------------- */
+
+/* Resource partitioning plan: DP groups per version in proportion to its
+ * workload (active plus pending requests).  A version with work keeps at least
+ * one group; the other groups go by the largest-remainder method on the
+ * quotas (n_groups - busy versions) * workload / total, equal remainders to the
+ * newer version; with no work, every group goes to the latest version.
+ *   workload    host int64 [n_versions], >= 0
+ *   groups_out  host int32 [n_versions], sums to n_groups
+ * DORA_ERR_INVALID_ARG for null pointers, negative workload, n_groups < 1, or
+ * more versions with work than groups. */
+dora_status dora_plan_partition(const int64_t* workload, int32_t n_versions, int32_t n_groups,
+                                int32_t* groups_out);
+
+/* Staleness-aware data supplementation: prompts to inject per version.  The
+ * latest version gets min(latest_quota, its idle slots), latest_quota being
+ * what its rollout batch still needs; every legacy version gets exactly its
+ * residual idle slots (groups * slots_per_group - active, at least 0).
+ *   groups, active  host int32 [n_versions], >= 0
+ *   inject_out      host int32 [n_versions] */
+dora_status dora_plan_supplement(const int32_t* groups, const int32_t* active,
+                                 int32_t n_versions, int32_t slots_per_group,
+                                 int64_t latest_quota, int32_t* inject_out);
+
+/* ---------------------------------------------------------------------------
  * Host page pool: page allocator plus per-version sequence tables for one
  * shared pool (Sec. 3.2: every request carries its version tag; Sec. 3.3: the
  * orchestrator reads per-version KV-cache utilisation; Sec. 3.4: migration

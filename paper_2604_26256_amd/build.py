@@ -23,7 +23,7 @@ LIB = os.path.join(PKG, "libdora.so")
 ARCH = "gfx950"
 
 HIP_SOURCES = ["decode.hip", "pack.hip", "append.hip"]
-CXX_SOURCES = ["api.cpp", "pool.cpp"]
+CXX_SOURCES = ["api.cpp", "pool.cpp", "plan.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

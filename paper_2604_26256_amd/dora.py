@@ -77,6 +77,11 @@ _lib.dora_decode_attn.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _
 _lib.dora_decode_attn.restype = ctypes.c_int
 _lib.dora_kv_append.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
 _lib.dora_kv_append.restype = ctypes.c_int
+_lib.dora_plan_partition.argtypes = [ctypes.POINTER(_I64), _I32, _I32, ctypes.POINTER(_I32)]
+_lib.dora_plan_partition.restype = ctypes.c_int
+_lib.dora_plan_supplement.argtypes = [ctypes.POINTER(_I32), ctypes.POINTER(_I32), _I32, _I32,
+                                      _I64, ctypes.POINTER(_I32)]
+_lib.dora_plan_supplement.restype = ctypes.c_int
 _lib.dora_kv_packed_bytes.argtypes = [_PackP, _I64]
 _lib.dora_kv_packed_bytes.restype = _SZ
 _lib.dora_kv_page_pack.argtypes = [_PackP, _P, _P, _P, _P, _P, _I64, _P, _SZ, _P]
@@ -326,6 +331,26 @@ def dora_kv_append(k_new, v_new, block_table, seq_lens, k_pages, v_pages, *, num
         _dev_ptr(page_owner, "page_owner", (torch.int16,), shape=(num_pages,), align=2)
     _check(_lib.dora_kv_append(ctypes.byref(desc), *args, _stream_handle(stream)),
            "dora_kv_append")
+
+
+def plan_partition(workload, n_groups):
+    """DP groups per policy version (oldest first) in proportion to workload."""
+    n = len(workload)
+    out = (ctypes.c_int32 * n)()
+    _check(_lib.dora_plan_partition((ctypes.c_int64 * n)(*[int(w) for w in workload]), n,
+                                    int(n_groups), out), "dora_plan_partition")
+    return list(out)
+
+
+def plan_supplement(groups, active, slots_per_group, latest_quota):
+    """Prompts to inject per version: latest first, legacy up to idle slots."""
+    n = len(groups)
+    out = (ctypes.c_int32 * n)()
+    _check(_lib.dora_plan_supplement((ctypes.c_int32 * n)(*[int(g) for g in groups]),
+                                     (ctypes.c_int32 * n)(*[int(a) for a in active]), n,
+                                     int(slots_per_group), int(latest_quota), out),
+           "dora_plan_supplement")
+    return list(out)
 
 
 # ---------------------------------------------------------------------------

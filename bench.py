@@ -194,6 +194,24 @@ def make_events(torch, n):
     return evs
 
 
+def time_calls(torch, fn, steps, warmup, flush):
+    """Per-call GPU time (ms) of fn, the cache evicted before each call.  The
+    events are made up front, so nothing in the loop waits for the GPU and the
+    flush hides the host's time to enqueue the call."""
+    for _ in range(warmup):
+        flush()
+        fn()
+    torch.cuda.synchronize()
+    starts, ends = make_events(torch, steps), make_events(torch, steps)
+    for i in range(steps):
+        flush()
+        starts[i].record()
+        fn()
+        ends[i].record()
+    torch.cuda.synchronize()
+    return [s.elapsed_time(e) for s, e in zip(starts, ends)]
+
+
 def time_decode(torch, dora, b, steps, warmup, flush, num_waves=0):
     """Returns dict of per-step and per-kernel timings (ms)."""
     w = b.w
@@ -257,6 +275,41 @@ def decode_record(w, lengths, t):
     }
 
 
+def time_grpo(torch, dora, steps, flush):
+    """The GRPO-shaped batch (16 responses per prompt sharing the prompt's full
+    pages): dora_decode_attn, which reads the shared pages once per member,
+    against dora_decode_attn_grouped, which reads them once per group."""
+    b, shared = wl.make_grpo_batch(device="cuda")
+    w, M = b.w, wl.GRPO_GROUP
+    plain = time_decode(torch, dora, b, steps, 2, flush)
+    out = torch.empty_like(b.q)
+    kw = dict(group_size=M,
+              num_kv_heads=w.num_kv_heads, page_size=w.page_size, kv_dtype=w.kv_dtype,
+              k_scales=b.k_scales, v_scales=b.v_scales)
+
+    def call():
+        dora.dora_decode_attn_grouped(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens,
+                                      b.version_ids, out, **kw)
+
+    ts = time_calls(torch, call, steps, 2, flush)
+    diff = (out.float() - plain["out"].float()).abs().max().item()
+    ab = wl.shared_prefix_algorithmic_bytes(w, b.lengths, shared, M)
+    rec = {"config": {"num_seqs": w.num_seqs, "group_size": M,
+                      "prompt_tokens": list(wl.GRPO_PROMPT),
+                      "heads": [w.num_q_heads, w.num_kv_heads], "head_dim": w.head_dim,
+                      "page_size": w.page_size, "kv_dtype": "bf16"},
+           "algorithmic_bytes": ab, "max_abs_diff_grouped_vs_plain": diff}
+    for name, ms in (("plain", float(np.median(plain["step_ms"]))),
+                     ("grouped", float(np.median(ts)))):
+        rec[name] = {"ms_per_step": ms,
+                     "decode_tokens_per_s": w.num_seqs / (ms * 1e-3),
+                     "gbps": ab["total"] / (ms * 1e-3) / 1e9,
+                     "frac_of_peak": ab["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+    rec["speedup"] = rec["plain"]["ms_per_step"] / rec["grouped"]["ms_per_step"]
+    del b
+    return rec
+
+
 def time_append(torch, dora, b, steps, flush):
     """KV append of one token per sequence (each sequence rewrites its last
     token, so every page it writes exists), cache evicted before each call."""
@@ -268,16 +321,8 @@ def time_append(torch, dora, b, steps, flush):
         torch.bfloat16)
     kw = dict(num_kv_heads=w.num_kv_heads, page_size=w.page_size, kv_dtype=w.kv_dtype,
               k_scales=b.k_scales, v_scales=b.v_scales)
-    ts = []
-    for i in range(steps + 2):
-        flush()
-        e0, e1 = make_events(torch, 2)
-        e0.record()
-        dora.dora_kv_append(kn, vn, b.block_table, b.seq_lens, b.k_pages, b.v_pages, **kw)
-        e1.record()
-        torch.cuda.synchronize()
-        if i >= 2:
-            ts.append(e0.elapsed_time(e1))
+    ts = time_calls(torch, lambda: dora.dora_kv_append(
+        kn, vn, b.block_table, b.seq_lens, b.k_pages, b.v_pages, **kw), steps, 2, flush)
     ab = wl.append_algorithmic_bytes(w, b.lengths)
     ms = float(np.median(ts))
     return {"ms": ms, "algorithmic_bytes": ab, "gbps": ab / (ms * 1e-3) / 1e9}
@@ -343,16 +388,7 @@ def time_offload(torch, dora, b, src_t, dst_t, packed, geo, n_seqs, moved, steps
             "h2d_copy": lambda: packed.copy_(host, non_blocking=True)}
     out = {}
     for name, fn in runs.items():
-        ts = []
-        for i in range(steps + 1):
-            flush()
-            e0, e1 = make_events(torch, 2)
-            e0.record()
-            fn()
-            e1.record()
-            torch.cuda.synchronize()
-            if i >= 1:
-                ts.append(e0.elapsed_time(e1))
+        ts = time_calls(torch, fn, steps, 1, flush)
         ms = float(np.median(ts))
         out[name + "_ms"] = ms
         out[name + "_gbps"] = moved / (ms * 1e-3) / 1e9
@@ -510,6 +546,13 @@ def main():
             del b
         torch.cuda.empty_cache()
 
+    grpo = None
+    if not args.only_main:
+        log("workload grpo7b (responses sharing prompt pages): timing")
+        grpo = time_grpo(torch, dora, max(5, args.steps // 3), flush)
+        log(f"workload grpo7b: {grpo['plain']['ms_per_step']:.4f} ms/step plain, "
+            f"{grpo['grouped']['ms_per_step']:.4f} grouped ({grpo['speedup']:.2f}x)")
+        torch.cuda.empty_cache()
     ref_rates = copy_bandwidth(torch)
     w = main_batch.w
     ab = main_rec["algorithmic_bytes"]["total"]
@@ -556,6 +599,7 @@ def main():
         "cpu_baseline": cpu,
         "flush_between_steps": None if args.no_flush else args.flush_mode,
         "workloads": results,
+        "shared_prefix": grpo,
     }
     print(json.dumps(line), flush=True)
 

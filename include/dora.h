@@ -158,6 +158,35 @@ dora_status dora_decode_attn(const dora_decode_desc* desc,
                              void* workspace, size_t workspace_bytes,
                              dora_stream_t stream);
 
+/* Decode attention for a batch made of response groups that share a prompt
+ * (the responses sampled per prompt for GRPO-style advantages, App. B).  The
+ * result equals dora_decode_attn's on the same arguments (up to fp32 rounding);
+ * what changes is that each group's shared prompt pages are read from HBM once
+ * instead of once per member.
+ *   group_size    M >= 1; sequences [k*M, (k+1)*M) form group k; num_seqs must
+ *                 be a multiple of M; M * (num_q_heads / num_kv_heads) <= 128
+ *                 (else DORA_ERR_UNSUPPORTED)
+ *   shared_pages_out  device int32 [num_seqs / M] or NULL: receives each
+ *                 group's shared prefix S_k (below)
+ *   other arguments as for dora_decode_attn; the workspace must hold
+ *   dora_decode_grouped_workspace_bytes(desc, group_size) bytes.
+ * Sharing is read off the block tables on the device: S_k is the number of
+ * leading pages that every member of group k holds in full (j < seq_len /
+ * page_size) under the same page id as the group's first member; a group of
+ * one shares nothing.  Any batch is valid input (S_k = 0 where nothing is
+ * shared).  Steps, all enqueued on `stream`, no host round trip: a plan kernel
+ * (S_k and each member's block-table row and length past it); a prefix kernel
+ * (per group, KV head and chunk of shared pages: pages staged in LDS once,
+ * applied to every member's query heads); the ordinary decode over each
+ * member's remaining pages, in fp32 with log-sum-exp; a merge kernel. */
+size_t dora_decode_grouped_workspace_bytes(const dora_decode_desc* desc, int32_t group_size);
+dora_status dora_decode_attn_grouped(const dora_decode_desc* desc, const void* q,
+                                     const void* k_pages, const void* v_pages,
+                                     const int32_t* block_table, const int32_t* seq_lens,
+                                     const int32_t* version_ids, void* out, int32_t group_size,
+                                     int32_t* shared_pages_out, void* workspace,
+                                     size_t workspace_bytes, dora_stream_t stream);
+
 /* Store every sequence's current-token K and V into its page slot: the write
  * that precedes each decode step (the per-token step of Sec. 2.2; seq_lens
  * counts that token, so dora_decode_attn with the same seq_lens then attends

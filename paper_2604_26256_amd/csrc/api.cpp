@@ -5,6 +5,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <vector>
+
 #include "dora_internal.h"
 
 using namespace dora;
@@ -107,6 +109,134 @@ size_t dora_decode_workspace_bytes(const dora_decode_desc* desc) {
   return w.total;
 }
 
+}  // extern "C"
+
+namespace dora {
+
+// DORA_FLAG_VALIDATE: range- and ownership-check every page id the call will
+// read, synchronously (err: one device int32 of scratch).
+dora_status validate_tables(const dora_decode_desc& d, const int32_t* block_table,
+                            const int32_t* seq_lens, const int32_t* version_ids, int32_t* err,
+                            hipStream_t s) {
+  if (launch_fill_i32(err, 0, 1, s) != hipSuccess) return DORA_ERR_HIP;
+  ValidateParams vp{block_table, seq_lens, version_ids, d.page_owner, d.num_seqs,
+                    d.page_size, d.block_table_stride, d.num_pages, err};
+  if (launch_validate(vp, s) != hipSuccess) return DORA_ERR_HIP;
+  int32_t host_err = 0;
+  if (hipMemcpyAsync(&host_err, err, 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return DORA_ERR_HIP;
+  return host_err ? DORA_ERR_DEVICE_CHECK : DORA_OK;
+}
+
+// Grouped decode: where each piece lives in the workspace (the decode
+// workspace first).  The shared prefixes are found on the device, so the
+// prefix launch and its partials are sized for the most chunks any group can
+// have: with chunk = clamp(ceil(S * K * Hkv / T), kPrefixMinChunk,
+// kPrefixMaxChunk), T = kPrefixTargetItems, and S <= stride, a (group, KV
+// head) has at most min(ceil(stride / kPrefixMinChunk),
+// max(ceil(T / (K * Hkv)), ceil(stride / kPrefixMaxChunk))) chunks.
+struct GroupedLayout {
+  WsLayout dec;
+  size_t gshared_off, part_o_off, part_ml_off, out32_off, lse_off, total;
+  int64_t cmax, items;
+};
+
+bool grouped_layout(const dora_decode_desc& d, int32_t group_size, GroupedLayout* L) {
+  const int64_t G = d.num_q_heads / d.num_kv_heads;
+  const int64_t n_groups = d.num_seqs / group_size;
+  const int64_t MG = group_size * G;
+  const int64_t kh = n_groups * d.num_kv_heads;
+  auto cdiv = [](int64_t a, int64_t b) { return (a + b - 1) / b; };
+  const int64_t lo = cdiv(d.block_table_stride, kPrefixMinChunk);
+  int64_t hi = kh > 0 ? cdiv(kPrefixTargetItems, kh) : 1;
+  const int64_t big = cdiv(d.block_table_stride, kPrefixMaxChunk);
+  hi = hi > big ? hi : big;
+  L->cmax = lo < hi ? lo : hi;
+  L->items = kh * L->cmax;
+  if (L->items > INT32_MAX / 2) return false;
+  if (!ws_layout(d, decode_waves(d), &L->dec)) return false;
+  size_t off = L->dec.total;
+  L->gshared_off = off;
+  off = align_up(off + (size_t)n_groups * 4);
+  L->part_o_off = off;
+  off = align_up(off + (size_t)L->items * MG * d.head_dim * 4);
+  L->part_ml_off = off;
+  off = align_up(off + (size_t)L->items * MG * 8);
+  L->out32_off = off;
+  off = align_up(off + (size_t)d.num_seqs * d.num_q_heads * d.head_dim * 4);
+  L->lse_off = off;
+  off = align_up(off + (size_t)d.num_seqs * d.num_q_heads * 4);
+  L->total = off;
+  return true;
+}
+
+// Host-checkable validity of the group arguments.
+dora_status check_groups(const dora_decode_desc& d, int32_t group_size) {
+  if (group_size < 1 || d.num_seqs % group_size != 0) return DORA_ERR_INVALID_ARG;
+  if ((int64_t)group_size * (d.num_q_heads / d.num_kv_heads) > 16 * kPrefixMaxWaves)
+    return DORA_ERR_UNSUPPORTED;
+  return DORA_OK;
+}
+
+// The decode launches of one call on validated arguments: per 8192 sequences,
+// the decode kernel and the combine kernel.  Outputs go to `out` (bf16), or,
+// when out32 is set (the grouped path's suffix), to out32 (fp32, normalised)
+// and lse (base-2 log-sum-exp), each sequence b starting at page
+// skip[b / skip_group].
+dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void* k_pages,
+                           const void* v_pages, const int32_t* block_table,
+                           const int32_t* seq_lens, uint16_t* out, float* out32, float* lse,
+                           const int32_t* skip, int32_t skip_group, uint8_t* ws,
+                           const WsLayout& w, hipStream_t s, hipEvent_t* ev) {
+  const bool fp8 = d.kv_dtype == DORA_KV_FP8_E4M3;
+  const int G = d.num_q_heads / d.num_kv_heads;
+  const int e = fp8 ? 1 : 2;
+  const float scale = d.sm_scale > 0.f ? d.sm_scale : 1.0f / sqrtf((float)d.head_dim);
+  const int64_t qrow = (int64_t)d.num_q_heads * d.head_dim;  // elements per sequence
+  if (ev && hipEventRecord(ev[0], s) != hipSuccess) return DORA_ERR_HIP;
+  for (int c0 = 0; c0 < d.num_seqs; c0 += kMaxSeqsPerLaunch) {
+    const int nb = d.num_seqs - c0 < kMaxSeqsPerLaunch ? d.num_seqs - c0 : kMaxSeqsPerLaunch;
+    DecodeParams dp;
+    dp.q = (const uint16_t*)q + c0 * qrow;
+    dp.k_pages = (const uint8_t*)k_pages;
+    dp.v_pages = (const uint8_t*)v_pages;
+    dp.k_scales = d.k_scales;
+    dp.v_scales = d.v_scales;
+    dp.block_table = block_table + (int64_t)c0 * d.block_table_stride;
+    dp.seq_lens = seq_lens + c0;
+    dp.out = out ? out + c0 * qrow : nullptr;
+    dp.out32 = out32 ? out32 + c0 * qrow : nullptr;
+    dp.lse = lse ? lse + (int64_t)c0 * d.num_q_heads : nullptr;
+    dp.skip = skip;
+    dp.skip_seq0 = c0;
+    dp.skip_group = skip_group;
+    dp.cuts = (int4*)(ws + w.cuts_off);
+    dp.part_o = (float*)(ws + w.part_o_off);
+    dp.part_ml = (float2*)(ws + w.part_ml_off);
+    dp.num_seqs = nb;
+    dp.num_q_heads = d.num_q_heads;
+    dp.num_kv_heads = d.num_kv_heads;
+    dp.group = G;
+    dp.stride = d.block_table_stride;
+    dp.min_range = min_range_of(d);
+    dp.page_bytes = (int64_t)d.num_kv_heads * d.page_size * d.head_dim * e;
+    dp.scale_log2 = scale * 1.4426950408889634f;
+    if (launch_decode(dp, d.head_dim, d.page_size, fp8, w.waves, s) != hipSuccess)
+      return DORA_ERR_HIP;
+    if (ev && c0 == 0 && hipEventRecord(ev[1], s) != hipSuccess) return DORA_ERR_HIP;
+    CombineParams cp{dp.cuts, dp.part_o, dp.part_ml, dp.out, dp.out32, dp.lse, d.num_q_heads, G,
+                     d.head_dim};
+    if (launch_combine(cp, w.waves, s) != hipSuccess) return DORA_ERR_HIP;
+  }
+  if (ev && hipEventRecord(ev[2], s) != hipSuccess) return DORA_ERR_HIP;
+  return DORA_OK;
+}
+
+}  // namespace dora
+
+extern "C" {
+
 dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const void* k_pages,
                              const void* v_pages, const int32_t* block_table,
                              const int32_t* seq_lens, const int32_t* version_ids, void* out,
@@ -131,55 +261,87 @@ dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const 
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace;
   hipEvent_t* ev = (hipEvent_t*)d.prof_events;
-  const int G = d.num_q_heads / d.num_kv_heads;
-  const int e = fp8 ? 1 : 2;
 
   if (validate) {
-    int32_t* err = (int32_t*)ws;
-    if (launch_fill_i32(err, 0, 1, s) != hipSuccess) return DORA_ERR_HIP;
-    ValidateParams vp{block_table, seq_lens, version_ids, d.page_owner, d.num_seqs,
-                      d.page_size, d.block_table_stride, d.num_pages, err};
-    if (launch_validate(vp, s) != hipSuccess) return DORA_ERR_HIP;
-    int32_t host_err = 0;
-    if (hipMemcpyAsync(&host_err, err, 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
-      return DORA_ERR_HIP;
-    if (host_err) return DORA_ERR_DEVICE_CHECK;
+    st = validate_tables(d, block_table, seq_lens, version_ids, (int32_t*)ws, s);
+    if (st != DORA_OK) return st;
   }
 
-  const float scale = d.sm_scale > 0.f ? d.sm_scale : 1.0f / sqrtf((float)d.head_dim);
-  const int64_t qrow = (int64_t)d.num_q_heads * d.head_dim;  // elements per sequence
-  if (ev && hipEventRecord(ev[0], s) != hipSuccess) return DORA_ERR_HIP;
-  for (int c0 = 0; c0 < d.num_seqs; c0 += kMaxSeqsPerLaunch) {
-    const int nb = d.num_seqs - c0 < kMaxSeqsPerLaunch ? d.num_seqs - c0 : kMaxSeqsPerLaunch;
-    DecodeParams dp;
-    dp.q = (const uint16_t*)q + c0 * qrow;
-    dp.k_pages = (const uint8_t*)k_pages;
-    dp.v_pages = (const uint8_t*)v_pages;
-    dp.k_scales = d.k_scales;
-    dp.v_scales = d.v_scales;
-    dp.block_table = block_table + (int64_t)c0 * d.block_table_stride;
-    dp.seq_lens = seq_lens + c0;
-    dp.out = (uint16_t*)out + c0 * qrow;
-    dp.cuts = (int4*)(ws + w.cuts_off);
-    dp.part_o = (float*)(ws + w.part_o_off);
-    dp.part_ml = (float2*)(ws + w.part_ml_off);
-    dp.num_seqs = nb;
-    dp.num_q_heads = d.num_q_heads;
-    dp.num_kv_heads = d.num_kv_heads;
-    dp.group = G;
-    dp.stride = d.block_table_stride;
-    dp.min_range = min_range_of(d);
-    dp.page_bytes = (int64_t)d.num_kv_heads * d.page_size * d.head_dim * e;
-    dp.scale_log2 = scale * 1.4426950408889634f;
-    if (launch_decode(dp, d.head_dim, d.page_size, fp8, w.waves, s) != hipSuccess)
-      return DORA_ERR_HIP;
-    if (ev && c0 == 0 && hipEventRecord(ev[1], s) != hipSuccess) return DORA_ERR_HIP;
-    CombineParams cp{dp.cuts, dp.part_o, dp.part_ml, dp.out, d.num_q_heads, G, d.head_dim};
-    if (launch_combine(cp, w.waves, s) != hipSuccess) return DORA_ERR_HIP;
+  return enqueue_decode(d, q, k_pages, v_pages, block_table, seq_lens, (uint16_t*)out, nullptr,
+                        nullptr, nullptr, 1, ws, w, s, ev);
+}
+
+size_t dora_decode_grouped_workspace_bytes(const dora_decode_desc* desc, int32_t group_size) {
+  if (check_desc(desc) != DORA_OK || check_groups(*desc, group_size) != DORA_OK) return 0;
+  GroupedLayout L;
+  if (!grouped_layout(*desc, group_size, &L)) return 0;
+  return L.total;
+}
+
+dora_status dora_decode_attn_grouped(const dora_decode_desc* desc, const void* q,
+                                     const void* k_pages, const void* v_pages,
+                                     const int32_t* block_table, const int32_t* seq_lens,
+                                     const int32_t* version_ids, void* out, int32_t group_size,
+                                     int32_t* shared_pages_out, void* workspace,
+                                     size_t workspace_bytes, dora_stream_t stream) {
+  dora_status st = check_desc(desc);
+  if (st != DORA_OK) return st;
+  const dora_decode_desc& d = *desc;
+  st = check_groups(d, group_size);
+  if (st != DORA_OK) return st;
+  if (d.num_seqs == 0) return DORA_OK;
+  const bool fp8 = d.kv_dtype == DORA_KV_FP8_E4M3;
+  if (!q || !k_pages || !v_pages || !block_table || !seq_lens || !out || !workspace)
+    return DORA_ERR_INVALID_ARG;
+  if (fp8 && (!d.k_scales || !d.v_scales)) return DORA_ERR_INVALID_ARG;
+  if ((d.flags & DORA_FLAG_VALIDATE) && !version_ids && d.page_owner)
+    return DORA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k_pages) || !aligned16(v_pages) || !aligned16(out) ||
+      !aligned16(workspace))
+    return DORA_ERR_INVALID_ARG;
+  GroupedLayout L;
+  if (!grouped_layout(d, group_size, &L)) return DORA_ERR_INVALID_ARG;
+  if (workspace_bytes < L.total) return DORA_ERR_WORKSPACE_TOO_SMALL;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* ws = (uint8_t*)workspace;
+  if (d.flags & DORA_FLAG_VALIDATE) {
+    st = validate_tables(d, block_table, seq_lens, version_ids, (int32_t*)ws, s);
+    if (st != DORA_OK) return st;
   }
-  if (ev && hipEventRecord(ev[2], s) != hipSuccess) return DORA_ERR_HIP;
-  return DORA_OK;
+
+  const int e = fp8 ? 1 : 2;
+  const float scale = d.sm_scale > 0.f ? d.sm_scale : 1.0f / sqrtf((float)d.head_dim);
+  GroupedParams gp;
+  gp.q = (const uint16_t*)q;
+  gp.k_pages = (const uint8_t*)k_pages;
+  gp.v_pages = (const uint8_t*)v_pages;
+  gp.k_scales = d.k_scales;
+  gp.v_scales = d.v_scales;
+  gp.block_table = block_table;
+  gp.seq_lens = seq_lens;
+  gp.group_shared = (int32_t*)(ws + L.gshared_off);
+  gp.shared_out = shared_pages_out;
+  gp.part_o = (float*)(ws + L.part_o_off);
+  gp.part_ml = (float2*)(ws + L.part_ml_off);
+  gp.out32 = (float*)(ws + L.out32_off);
+  gp.lse = (float*)(ws + L.lse_off);
+  gp.out = (uint16_t*)out;
+  gp.num_seqs = d.num_seqs;
+  gp.num_q_heads = d.num_q_heads;
+  gp.num_kv_heads = d.num_kv_heads;
+  gp.group = d.num_q_heads / d.num_kv_heads;
+  gp.stride = d.block_table_stride;
+  gp.group_size = group_size;
+  gp.page_size = d.page_size;
+  gp.head_dim = d.head_dim;
+  gp.cmax = (int32_t)L.cmax;
+  gp.page_bytes = (int64_t)d.num_kv_heads * d.page_size * d.head_dim * e;
+  gp.scale_log2 = scale * 1.4426950408889634f;
+  if (launch_grouped_prefix(gp, (int)L.items, fp8, s) != hipSuccess) return DORA_ERR_HIP;
+  st = enqueue_decode(d, q, k_pages, v_pages, block_table, seq_lens, nullptr, gp.out32, gp.lse,
+                      gp.group_shared, group_size, ws, L.dec, s, nullptr);
+  if (st != DORA_OK) return st;
+  return launch_grouped_merge(gp, s) == hipSuccess ? DORA_OK : DORA_ERR_HIP;
 }
 
 dora_status dora_kv_append(const dora_decode_desc* desc, const void* k_new, const void* v_new,

@@ -41,16 +41,10 @@
 
 #include <type_traits>
 
+#include "decode_core.h"
 #include "dora_internal.h"
 
 namespace dora {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------------------
 // shared helpers
@@ -95,66 +89,6 @@ struct Split {
   }
 };
 
-// ---------------------------------------------------------------------------
-// decode
-// ---------------------------------------------------------------------------
-
-// Raw bytes of one page's K and V tiles for one KV head, as each lane loads them.
-template <int D, int P, bool FP8>
-struct PageRegs {
-  static constexpr int NT = P / 16;                               // 16-token sub-tiles
-  static constexpr int NK = FP8 ? NT * (D / 64) : NT * (D / 32);  // 16-byte K loads
-  static constexpr int VB = (P == 16 ? 4 : 8) * (FP8 ? 1 : 2);    // bytes per V load
-  u32x4 k[NK];
-  typedef typename std::conditional<
-      VB == 16, u32x4, typename std::conditional<VB == 8, u32x2, uint32_t>::type>::type vraw_t;
-  vraw_t v[D / 16];
-};
-
-// Token slot (within the page) that MFMA row r of sub-tile t holds.  With 32-token
-// pages the rows interleave so that the QK^T accumulator rows of lane row-group
-// q are tokens 8q..8q+7, exactly the k-range that lane supplies to the PV MFMA.
-template <int P>
-__device__ __forceinline__ int tile_token(int t, int r) {
-  return P == 16 ? r : 8 * (r >> 2) + 4 * t + (r & 3);
-}
-
-__device__ __forceinline__ bf16x8 fp8x8_to_bf16(uint32_t w0, uint32_t w1) {
-  const bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, false);
-  const bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, true);
-  const bf16x2 c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w1, 1.0f, false);
-  const bf16x2 d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w1, 1.0f, true);
-  return bf16x8{a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
-}
-
-__device__ __forceinline__ bf16x4 fp8x4_to_bf16(uint32_t w0) {
-  const bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, false);
-  const bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, true);
-  return bf16x4{a[0], a[1], b[0], b[1]};
-}
-
-// K: lane reads token tile_token(t, col) of 16-byte chunk (4s + grp); the chunk
-// and sub-tile strides are compile-time constants, so every K load is the
-// lane's base offset plus an immediate.  V: 16 head-dim rows per load, rows
-// 16 * P elements apart.  Every KV byte is read once per call, so the loads
-// are non-temporal (no cache allocation for streaming data).
-template <int D, int P, bool FP8>
-__device__ __forceinline__ void load_page(PageRegs<D, P, FP8>& r, const uint8_t* kbase,
-                                          const uint8_t* vbase, uint32_t koff, uint32_t voff) {
-  typedef PageRegs<D, P, FP8> R;
-  constexpr int per_t = R::NK / R::NT;
-#pragma unroll
-  for (int t = 0; t < R::NT; ++t)
-#pragma unroll
-    for (int s = 0; s < per_t; ++s)
-      r.k[t * per_t + s] =
-          __builtin_nontemporal_load((const u32x4*)(kbase + koff + (4 * s * P + 4 * t) * 16));
-  constexpr int vrow = P * (FP8 ? 1 : 2) * 16;  // bytes between 16-row blocks of V
-#pragma unroll
-  for (int i = 0; i < D / 16; ++i)
-    r.v[i] = __builtin_nontemporal_load((const typename R::vraw_t*)(vbase + voff + i * vrow));
-}
-
 // Page-head descriptor word: j (19 bits) | g << 19 (7 bits) | last << 26 |
 // (tokens valid in the page - 1) << 27.
 __device__ __forceinline__ int desc_j(uint32_t d) { return (int)(d & 0x7FFFFu); }
@@ -162,7 +96,12 @@ __device__ __forceinline__ int desc_g(uint32_t d) { return (int)((d >> 19) & 0x7
 __device__ __forceinline__ bool desc_last(uint32_t d) { return (d >> 26) & 1u; }
 __device__ __forceinline__ int desc_nvalid(uint32_t d) { return (int)(d >> 27) + 1; }
 
-template <int D, int P, bool FP8, int NBUF>
+// SUFFIX: the decode of the grouped path.  Each sequence starts after the
+// pages its group shares (skip[(skip_seq0 + b) / skip_group] pages, which the
+// group-prefix kernel covers), and the kernel writes normalised fp32 rows and
+// their log-sum-exp (out32, lse) instead of bf16 rows.  A separate
+// instantiation, so the plain kernel is unchanged.
+template <int D, int P, bool FP8, int NBUF, bool SUFFIX>
 __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   typedef PageRegs<D, P, FP8> R;
   constexpr int NT = R::NT;
@@ -187,6 +126,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
     for (int k = 0; k < 8; ++k) {
       const int b = base + lane * 8 + k;
       n[k] = b < B ? pages_of(p.seq_lens[b], P, p.stride) : 0;
+      if constexpr (SUFFIX) n[k] -= b < B ? p.skip[(p.skip_seq0 + b) / p.skip_group] : 0;
       tsum += n[k];
     }
     const int incl = wave_inclusive_scan(tsum);
@@ -205,6 +145,12 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   // empty sequences: zero output, shared out over the launched wavefronts
   for (int b = (int)w; b < B; b += gridDim.x) {
     if (sN[b + 1] != sN[b]) continue;
+    if constexpr (SUFFIX) {  // fp32 outputs: zero, and an empty softmax (lse -inf)
+      float* o = p.out32 + (int64_t)b * Hq * D;
+      for (int e = lane; e < Hq * D; e += 64) o[e] = 0.f;
+      for (int e = lane; e < Hq; e += 64) p.lse[(int64_t)b * Hq + e] = -__builtin_inff();
+      continue;
+    }
     uint32_t* o = (uint32_t*)(p.out + (int64_t)b * Hq * D);
     for (int e = lane; e < Hq * D / 2; e += 64) o[e] = 0u;
   }
@@ -238,10 +184,11 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
       const int r = x - Hkv * sN[lo];
       const int g = r / nb;
       const int j = r - g * nb;
-      int nv = p.seq_lens[lo] - j * P;
+      const int jt = SUFFIX ? j + p.skip[(p.skip_seq0 + lo) / p.skip_group] : j;  // table index
+      int nv = p.seq_lens[lo] - jt * P;
       nv = nv > P ? P : nv;
       db = lo;
-      dpid = p.block_table[(int64_t)lo * p.stride + j];
+      dpid = p.block_table[(int64_t)lo * p.stride + jt];
       dinfo = (uint32_t)j | ((uint32_t)g << 19) | ((uint32_t)(j == nb - 1) << 26) |
               ((uint32_t)(nv - 1) << 27);
     }
@@ -263,12 +210,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   // Query operand of (b, g): lane supplies q[head col][8 head-dim values] per
   // k-step, in the head-dim order the K chunks are consumed in.
   auto load_q = [&](bf16x8(&dst)[KSTEPS], int b, int g) {
-    const uint16_t* qrow = p.q + ((int64_t)b * Hq + (int64_t)g * G + col) * D;
-#pragma unroll
-    for (int s = 0; s < KSTEPS; ++s) {
-      const int d0 = FP8 ? 64 * (s >> 1) + 16 * grp + 8 * (s & 1) : 32 * s + 8 * grp;
-      dst[s] = col < G ? *(const bf16x8*)(qrow + d0) : bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
-    }
+    load_q_operand<D, FP8>(dst, p.q + ((int64_t)b * Hq + (int64_t)g * G + col) * D, col < G);
   };
   // The query of the next segment is fetched together with that segment's
   // first page (q_next, tagged with the page-head where the segment starts).
@@ -300,12 +242,20 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
     if (col < G) {
       if (seg_whole) {
         const float inv = 1.f / l_tot;
-        uint16_t* o = p.out + ((int64_t)seg_b * Hq + seg_g * G + col) * D + 4 * grp;
+        const int64_t row = (int64_t)seg_b * Hq + seg_g * G + col;
+        if constexpr (SUFFIX) {  // normalised fp32 output and its base-2 log-sum-exp
 #pragma unroll
-        for (int i = 0; i < DBLK; ++i)
-          *(bf16x4*)(o + 16 * i) =
-              bf16x4{(__bf16)(acc[i][0] * inv), (__bf16)(acc[i][1] * inv),
-                     (__bf16)(acc[i][2] * inv), (__bf16)(acc[i][3] * inv)};
+          for (int i = 0; i < DBLK; ++i)
+            *(f32x4*)(p.out32 + row * D + 4 * grp + 16 * i) = acc[i] * inv;
+          if (grp == 0) p.lse[row] = m_run + __builtin_amdgcn_logf(l_tot);
+        } else {
+          uint16_t* o = p.out + row * D + 4 * grp;
+#pragma unroll
+          for (int i = 0; i < DBLK; ++i)
+            *(bf16x4*)(o + 16 * i) =
+                bf16x4{(__bf16)(acc[i][0] * inv), (__bf16)(acc[i][1] * inv),
+                       (__bf16)(acc[i][2] * inv), (__bf16)(acc[i][3] * inv)};
+        }
       } else {
         const int64_t slot = 2 * w + (first_seg ? 0 : 1);
         float* po = p.part_o + (slot * G + col) * D + 4 * grp;
@@ -325,91 +275,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   };
 
   auto consume = [&](const R& r, int nvalid, float ksc, float vsc) {
-    // scores S^T: lane holds tokens of its row group for head `col`
-    f32x4 sc[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks) {
-        bf16x8 a;
-        if constexpr (FP8) {
-          const u32x4& wd = r.k[t * (D / 64) + (ks >> 1)];
-          a = (ks & 1) ? fp8x8_to_bf16(wd[2], wd[3]) : fp8x8_to_bf16(wd[0], wd[1]);
-        } else {
-          a = __builtin_bit_cast(bf16x8, r.k[t * KSTEPS + ks]);
-        }
-        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[ks], s, 0, 0, 0);
-      }
-      sc[t] = s;
-    }
-    float mx = -__builtin_inff();
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float x = sc[t][i] * ksc;
-        const int tok = P == 16 ? 4 * grp + i : 8 * grp + 4 * t + i;
-        if (nvalid < P && tok >= nvalid) x = -__builtin_inff();
-        sc[t][i] = x;
-        mx = fmaxf(mx, x);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    float psum = 0.f;
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float e = __builtin_amdgcn_exp2f(sc[t][i] - m_new);
-        psum += e;
-        sc[t][i] = e * vsc;
-      }
-    l_run = l_run * alpha + psum;
-    if (__ballot(alpha != 1.f)) {
-#pragma unroll
-      for (int i = 0; i < DBLK; ++i) acc[i] *= alpha;
-    }
-    // P^T operand, then O^T += V^T P^T per 16-row block of the head dim
-    if constexpr (P == 16) {
-      const bf16x4 pb4 = bf16x4{(__bf16)sc[0][0], (__bf16)sc[0][1], (__bf16)sc[0][2],
-                                (__bf16)sc[0][3]};
-#pragma unroll
-      for (int i = 0; i < DBLK; ++i) {
-        bf16x4 a;
-        if constexpr (FP8)
-          a = fp8x4_to_bf16(r.v[i]);
-        else
-          a = __builtin_bit_cast(bf16x4, r.v[i]);
-        if (nvalid < P) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (4 * grp + e >= nvalid) a[e] = (__bf16)0.f;
-        }
-        acc[i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, pb4, acc[i], 0, 0, 0);
-      }
-    } else {
-      const bf16x8 pb8 = bf16x8{(__bf16)sc[0][0], (__bf16)sc[0][1], (__bf16)sc[0][2],
-                                (__bf16)sc[0][3], (__bf16)sc[1][0], (__bf16)sc[1][1],
-                                (__bf16)sc[1][2], (__bf16)sc[1][3]};
-#pragma unroll
-      for (int i = 0; i < DBLK; ++i) {
-        bf16x8 a;
-        if constexpr (FP8)
-          a = fp8x8_to_bf16(r.v[i][0], r.v[i][1]);
-        else
-          a = __builtin_bit_cast(bf16x8, r.v[i]);
-        if (nvalid < P) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (8 * grp + e >= nvalid) a[e] = (__bf16)0.f;
-        }
-        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb8, acc[i], 0, 0, 0);
-      }
-    }
+    consume_page<D, P, FP8>(r, nvalid, ksc, vsc, qop, acc, m_run, l_run);
   };
 
   // 3. stream the range.  Descriptors come in chunks of 64 (current and next);
@@ -563,9 +429,15 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(CombineParams 
       den += sc * sS[i];
     }
     const float inv = 1.f / den;
-    uint16_t* o = p.out + ((int64_t)b * p.num_q_heads + g * G + n) * D + 4 * d4;
-    *(bf16x4*)o = bf16x4{(__bf16)(num[0] * inv), (__bf16)(num[1] * inv),
-                         (__bf16)(num[2] * inv), (__bf16)(num[3] * inv)};
+    const int64_t row = (int64_t)b * p.num_q_heads + g * G + n;
+    if (p.out32) {
+      *(f32x4*)(p.out32 + row * D + 4 * d4) = num * inv;
+      if (d4 == 0) p.lse[row] = Mx + __builtin_amdgcn_logf(den);
+    } else {
+      uint16_t* o = p.out + row * D + 4 * d4;
+      *(bf16x4*)o = bf16x4{(__bf16)(num[0] * inv), (__bf16)(num[1] * inv),
+                           (__bf16)(num[2] * inv), (__bf16)(num[3] * inv)};
+    }
   }
 }
 
@@ -609,24 +481,27 @@ constexpr int page_buffers() {
 }
 
 template <int D, int P, bool FP8>
-static const void* decode_fn() {
-  return (const void*)&decode_kernel<D, P, FP8, page_buffers<D, P, FP8>()>;
+static const void* decode_fn(bool out32) {
+  constexpr int NBUF = page_buffers<D, P, FP8>();
+  return out32 ? (const void*)&decode_kernel<D, P, FP8, NBUF, true>
+               : (const void*)&decode_kernel<D, P, FP8, NBUF, false>;
 }
 
-static const void* decode_symbol(int head_dim, int page_size, bool fp8) {
+static const void* decode_symbol(int head_dim, int page_size, bool fp8, bool out32) {
   if (head_dim == 128) {
-    if (page_size == 16) return fp8 ? decode_fn<128, 16, true>() : decode_fn<128, 16, false>();
-    return fp8 ? decode_fn<128, 32, true>() : decode_fn<128, 32, false>();
+    if (page_size == 16)
+      return fp8 ? decode_fn<128, 16, true>(out32) : decode_fn<128, 16, false>(out32);
+    return fp8 ? decode_fn<128, 32, true>(out32) : decode_fn<128, 32, false>(out32);
   }
-  if (page_size == 16) return fp8 ? decode_fn<64, 16, true>() : decode_fn<64, 16, false>();
-  return fp8 ? decode_fn<64, 32, true>() : decode_fn<64, 32, false>();
+  if (page_size == 16) return fp8 ? decode_fn<64, 16, true>(out32) : decode_fn<64, 16, false>(out32);
+  return fp8 ? decode_fn<64, 32, true>(out32) : decode_fn<64, 32, false>(out32);
 }
 
 size_t decode_lds_bytes(int num_seqs) { return (size_t)(num_seqs + 1) * sizeof(int); }
 
 hipError_t decode_waves_per_cu(int head_dim, int page_size, bool fp8, int num_seqs, int* out) {
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(
-      out, decode_symbol(head_dim, page_size, fp8), 64, decode_lds_bytes(num_seqs));
+      out, decode_symbol(head_dim, page_size, fp8, false), 64, decode_lds_bytes(num_seqs));
 }
 
 hipError_t launch_decode(const DecodeParams& p, int head_dim, int page_size, bool fp8,
@@ -634,7 +509,8 @@ hipError_t launch_decode(const DecodeParams& p, int head_dim, int page_size, boo
   if (waves <= 0) return hipSuccess;
   DecodeParams arg = p;
   void* args[] = {(void*)&arg};
-  return hipLaunchKernel(decode_symbol(head_dim, page_size, fp8), dim3((unsigned)waves),
+  return hipLaunchKernel(decode_symbol(head_dim, page_size, fp8, p.out32 != nullptr),
+                         dim3((unsigned)waves),
                          dim3(64), args, decode_lds_bytes(p.num_seqs), s);
 }
 

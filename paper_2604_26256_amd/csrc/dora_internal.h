@@ -46,6 +46,10 @@ struct DecodeParams {
   const int32_t* block_table;
   const int32_t* seq_lens;
   uint16_t* out;
+  float* out32;        // if set: normalised fp32 output [B][Hq][d] instead of `out`,
+  float* lse;          // with each row's base-2 log-sum-exp [B][Hq] (scores in log2 units),
+  const int32_t* skip; // and sequence b starts at page skip[(skip_seq0 + b) / skip_group]
+  int32_t skip_seq0, skip_group;
   int4* cuts;          // per wavefront: {b, g, pieces, first-slot offset} or b = -1
   float* part_o;
   float2* part_ml;
@@ -60,8 +64,45 @@ struct CombineParams {
   const float* part_o;
   const float2* part_ml;
   uint16_t* out;
+  float* out32;  // as in DecodeParams
+  float* lse;
   int32_t num_q_heads, group, head_dim;
 };
+
+// Grouped decode (groups of sequences sharing a prompt's pages).
+constexpr int kPrefixMaxWaves = 8;      // (member, head) columns per group <= 128
+constexpr int kPrefixMinChunk = 16;     // shared pages per prefix work item, at least ...
+constexpr int kPrefixMaxChunk = 512;    // ... and at most
+constexpr int kPrefixTargetItems = 512; // prefix work items aimed at (2 per CU)
+
+struct GroupedParams {
+  const uint16_t* q;
+  const uint8_t* k_pages;
+  const uint8_t* v_pages;
+  const float* k_scales;
+  const float* v_scales;
+  const int32_t* block_table;
+  const int32_t* seq_lens;
+  int32_t* group_shared;      // per group: shared full pages (prefix kernel)
+  int32_t* shared_out;        // optional caller copy of group_shared
+  float* part_o;              // [items][columns][d] unnormalised prefix partials
+  float2* part_ml;            // [items][columns] {max (log2 units), sum}
+  float* out32;               // suffix rows [B][Hq][d] (normalised) ...
+  float* lse;                 // ... and their base-2 log-sum-exp [B][Hq]
+  uint16_t* out;
+  int32_t num_seqs, num_q_heads, num_kv_heads, group, stride, group_size, page_size, head_dim;
+  int32_t cmax;               // prefix items per (group, KV head), at most
+  int64_t page_bytes;
+  float scale_log2;
+};
+
+hipError_t launch_grouped_prefix(const GroupedParams& p, int grid, bool fp8, hipStream_t s);
+hipError_t launch_grouped_merge(const GroupedParams& p, hipStream_t s);
+dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void* k_pages,
+                           const void* v_pages, const int32_t* block_table,
+                           const int32_t* seq_lens, uint16_t* out, float* out32, float* lse,
+                           const int32_t* skip, int32_t skip_group, uint8_t* ws,
+                           const WsLayout& w, hipStream_t s, hipEvent_t* ev);
 
 struct ValidateParams {
   const int32_t* block_table;

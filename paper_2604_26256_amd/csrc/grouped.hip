@@ -1,0 +1,313 @@
+// Decode attention for batches of response groups that share a prompt (the
+// GRPO groups of the paper's rollouts: several responses sampled per prompt,
+// App. B).  Within a group the members' block tables start with the same page
+// ids for the prompt's full pages.  Those shared pages are read from HBM once
+// per group instead of once per member.  Everything is planned on the device
+// from the block tables, so a call makes no host round trip:
+//
+//   prefix   one workgroup per (group, KV head, chunk of the group's shared
+//            pages).  It finds the group's shared prefix S (leading page ids
+//            equal in every member's row, full pages of every member), then
+//            its waves stage the pages' K and V tiles in LDS (double-buffered,
+//            one barrier per step); wave t applies them to 16 of the group's
+//            (member, query head) columns with the same MFMA/online-softmax
+//            step as the decode kernel, and writes an unnormalised partial
+//            (o, running max, sum) per column.
+//   suffix   the decode kernel over each member's pages past S, writing fp32
+//            rows and their log-sum-exp.
+//   merge    per (sequence, KV head): the chunk partials of its prefix and its
+//            suffix row folded into the bf16 output.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "decode_core.h"
+#include "dora_internal.h"
+
+namespace dora {
+
+constexpr int kPrefixThreads = 64 * kPrefixMaxWaves;
+constexpr int kStageSets = 2;  // steps in flight per workgroup (register staging)
+
+// Shared prefix of group k (all threads of the workgroup get it): the number
+// of leading pages that every member holds in full (floor(len / P), at most
+// the table's width) and whose page id equals the leader's; a group of one
+// shares nothing.  Returns early, with a value <= `enough`, once every member's
+// full pages number at most `enough`.
+__device__ int shared_prefix(const GroupedParams& p, int k, int enough) {
+  __shared__ int s_cap, s_min;
+  const int M = p.group_size, P = p.page_size, stride = p.stride;
+  const int64_t b0 = (int64_t)k * M;
+  if (M == 1) return 0;
+  if (threadIdx.x == 0) s_cap = s_min = stride;
+  __syncthreads();
+  if ((int)threadIdx.x < M) {
+    const int L = p.seq_lens[b0 + threadIdx.x];
+    atomicMin(&s_cap, L > 0 ? L / P : 0);
+  }
+  __syncthreads();
+  const int cap = s_cap;  // final here; mismatches go to s_min
+  if (cap <= enough) return cap;
+  const int32_t* __restrict__ lead = p.block_table + b0 * stride;
+  int first = cap;  // this thread's smallest mismatch; no atomics inside the
+#pragma unroll 4  // loop, so its loads issue back to back
+  for (int x = threadIdx.x; x < (M - 1) * cap; x += blockDim.x) {
+    const int m = 1 + x / cap, j = x - (m - 1) * cap;
+    if (p.block_table[(b0 + m) * stride + j] != lead[j]) first = j < first ? j : first;
+  }
+  if (first < cap) atomicMin(&s_min, first);
+  __syncthreads();
+  return s_min < cap ? s_min : cap;
+}
+
+// Pages per prefix work item of a group sharing S pages: about
+// kPrefixTargetItems items over all K * Hkv (group, KV head) pairs, clamped to
+// [kPrefixMinChunk, kPrefixMaxChunk].  Item (k, g, c) covers pages
+// [c * chunk, min((c + 1) * chunk, S)); its partials sit at item index
+// (k * Hkv + g) * cmax + c.  The prefix and merge kernels both derive the
+// split from here.
+__device__ __forceinline__ int prefix_chunk(int S, const GroupedParams& p) {
+  const int64_t kh = (int64_t)(p.num_seqs / p.group_size) * p.num_kv_heads;
+  const int64_t want = ((int64_t)S * kh + kPrefixTargetItems - 1) / kPrefixTargetItems;
+  return want < kPrefixMinChunk ? kPrefixMinChunk
+                                : (want > kPrefixMaxChunk ? kPrefixMaxChunk : (int)want);
+}
+
+// One step consumes PAIR consecutive pages as one virtual page of VP = PAIR * P
+// tokens (bf16 16-token pages go in pairs: half the softmax reductions and
+// barriers; fp8 pages keep their own scales, one page per step).  LDS holds a
+// step in the layout of a VP-token page, so the decode's lane operands apply:
+// K [d/8][VP][8] and V [d][VP] for bf16.
+template <int D, int P, bool FP8>
+__global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(GroupedParams p) {
+  constexpr int PAIR = (!FP8 && P == 16) ? 2 : 1;
+  constexpr int VP = PAIR * P;
+  typedef PageRegs<D, VP, FP8> R;
+  typedef typename R::vraw_t vraw_t;
+  constexpr int E = FP8 ? 1 : 2;
+  constexpr int TILE = P * D * E;  // bytes of one (page, KV head) K tile; V's is the same
+  constexpr int PIECES = 2 * PAIR * TILE / 16;  // 16-byte pieces per step
+  constexpr int PER = (PIECES + kPrefixThreads - 1) / kPrefixThreads;
+  constexpr int per_t = R::NK / R::NT;
+  // V rows in LDS are padded by 16 bytes where the lanes' row-strided reads
+  // would otherwise meet in the same banks.
+  constexpr int VROW = VP * E >= 32 ? VP * E + 16 : VP * E;
+  constexpr int vrow = 16 * VROW;                 // bytes between 16-row blocks of V
+  constexpr int KBYTES = PAIR * TILE;             // K part of a step in LDS
+  __shared__ __align__(16) uint8_t lds[2][KBYTES + D * VROW];
+  __shared__ int s_pid[kPrefixMaxChunk];
+  __shared__ float s_ksc[FP8 ? kPrefixMaxChunk : 1], s_vsc[FP8 ? kPrefixMaxChunk : 1];
+
+  // chunk-major order: the blocks that have work (low chunk indices) come
+  // first and are dispatched first
+  const int KH = p.num_seqs / p.group_size * p.num_kv_heads;
+  const int c = blockIdx.x / KH, kg = blockIdx.x - c * KH;
+  const int k = kg / p.num_kv_heads, g = kg - k * p.num_kv_heads;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = lane & 15, grp = lane >> 4;
+  const int G = p.group, MG = p.group_size * G;
+  const bool computes = wave * 16 < MG;  // waves past the columns only help staging
+  const int cg = wave * 16 + col;        // this lane's column among (member, head) pairs
+  const bool active = cg < MG;
+  const int m = active ? cg / G : 0, h = active ? cg - m * G : 0;
+  const int64_t b = (int64_t)k * p.group_size + m;
+
+  bf16x8 qop[D / 32];  // issued first: it does not depend on the prefix
+  load_q_operand<D, FP8>(qop, p.q + (b * p.num_q_heads + (int64_t)g * G + h) * D, active);
+
+  // The group's shared prefix; the first workgroup of each group publishes it
+  // for the suffix decode and the merge.  A chunk that starts past every
+  // member's full pages has no work whatever the prefix is.
+  const int S = shared_prefix(p, k, c * kPrefixMinChunk);
+  if (c == 0 && g == 0 && threadIdx.x == 0) {
+    p.group_shared[k] = S;
+    if (p.shared_out) p.shared_out[k] = S;
+  }
+  const int chunk = prefix_chunk(S, p);
+  const int j0 = c * chunk;
+  if (j0 >= S) return;  // uniform: this chunk is past the group's prefix
+  const int j1 = j0 + chunk < S ? j0 + chunk : S;
+  // The item's page ids (and fp8 scales) go to LDS first: a page load that
+  // waited on a block-table load would wait on every load issued before it.
+  f32x4 acc[D / 16];
+#pragma unroll
+  for (int i = 0; i < D / 16; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -__builtin_inff(), l_run = 0.f;
+
+  const int32_t* bt = p.block_table + (int64_t)k * p.group_size * p.stride;  // the leader's row
+  for (int t = threadIdx.x; t < j1 - j0; t += kPrefixThreads) {
+    const int pid = bt[j0 + t];
+    s_pid[t] = pid;
+    if constexpr (FP8) {
+      s_ksc[t] = p.scale_log2 * p.k_scales[pid];
+      s_vsc[t] = p.v_scales[pid];
+    }
+  }
+  __syncthreads();
+  const uint32_t koff = (uint32_t)((grp * VP + tile_token<VP>(0, col)) * 16);
+  const uint32_t voff = (uint32_t)(col * VROW + (VP == 16 ? 4 : 8) * grp * E);
+
+  // Piece o of a step: page h = o / (2 TILE / 16) of the step, then its K tile
+  // and V tile in 16-byte pieces.  lds_of maps it into the VP-token layout.
+  auto lds_of = [&](int o) -> int {
+    const int hh = o / (2 * TILE / 16), w = o - hh * (2 * TILE / 16);
+    if (w < TILE / 16) {  // K piece (dx, token) -> (dx, hh * P + token)
+      const int dx = w / P, t = w - dx * P;
+      return (dx * VP + hh * P + t) * 16;
+    }
+    constexpr int RP = P * E / 16 > 0 ? P * E / 16 : 1;  // 16-byte pieces per V row of a page
+    const int v = w - TILE / 16;  // V piece (row, r) -> row of the step, after page hh
+    const int row = v / RP;
+    return KBYTES + row * VROW + hh * P * E + (v - row * RP) * 16;
+  };
+  // Loads are never skipped, so the compiler's in-order wait counts stay exact
+  // (a load under a branch makes it wait for everything): a step past the end
+  // re-reads the last step, a missing second page re-reads the last page, and
+  // pieces past the step (fp8 16-token pages) re-read an earlier piece.  None
+  // of these duplicates reach a score: LDS only takes the real pieces, and the
+  // tokens of a missing page are masked.
+  u32x4 st[kStageSets][PER];
+  const int n_steps = (j1 - j0 + PAIR - 1) / PAIR;
+  auto fetch = [&](u32x4(&dst)[PER], int step) {
+    step = step < n_steps ? step : n_steps - 1;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int o = (threadIdx.x + i * kPrefixThreads) % PIECES;
+      const int hh = o / (2 * TILE / 16), w = (o - hh * (2 * TILE / 16)) * 16;
+      int j = j0 + step * PAIR + hh;
+      j = j < j1 ? j : j1 - 1;
+      const int64_t pid = s_pid[j - j0];
+      const uint8_t* src = (w < TILE ? p.k_pages + w : p.v_pages + (w - TILE)) +
+                           pid * p.page_bytes + (int64_t)g * TILE;
+      dst[i] = *(const u32x4*)src;
+    }
+  };
+  auto put = [&](const u32x4(&src)[PER], int buf, int step) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int o = threadIdx.x + i * kPrefixThreads;
+      const int j = j0 + step * PAIR + o / (2 * TILE / 16);
+      if (o < PIECES && j < j1) *(u32x4*)&lds[buf][lds_of(o)] = src[i];
+    }
+  };
+
+#pragma unroll
+  for (int r = 0; r < kStageSets; ++r) fetch(st[r], r);
+  put(st[0], 0, 0);
+  __syncthreads();
+  for (int base = 0; base < n_steps; base += kStageSets) {
+#pragma unroll
+    for (int r = 0; r < kStageSets; ++r) {
+      const int u = base + r;  // step u sits in LDS buffer u & 1; its register set r is free
+      fetch(st[r], u + kStageSets);
+      if (u < n_steps) {
+        if (computes) {
+          const int buf = u & 1;
+          R pr;
+#pragma unroll
+          for (int t = 0; t < R::NT; ++t)
+#pragma unroll
+            for (int s = 0; s < per_t; ++s)
+              pr.k[t * per_t + s] = *(const u32x4*)&lds[buf][koff + (4 * s * VP + 4 * t) * 16];
+#pragma unroll
+          for (int i = 0; i < D / 16; ++i)
+            pr.v[i] = *(const vraw_t*)&lds[buf][KBYTES + voff + i * vrow];
+          const int jj = j0 + u * PAIR;
+          float ksc = p.scale_log2, vsc = 1.f;
+          if constexpr (FP8) {
+            ksc = s_ksc[jj - j0];
+            vsc = s_vsc[jj - j0];
+          }
+          const int nvalid = (j1 - jj < PAIR ? j1 - jj : PAIR) * P;  // shared pages are full
+          consume_page<D, VP, FP8>(pr, nvalid, ksc, vsc, qop, acc, m_run, l_run);
+        }
+        if (u + 1 < n_steps) put(st[(r + 1) % kStageSets], (u + 1) & 1, u + 1);
+        __syncthreads();
+      }
+    }
+  }
+
+  float l_tot = l_run + __shfl_xor(l_run, 16);
+  l_tot += __shfl_xor(l_tot, 32);
+  if (active) {
+    const int64_t slot = ((int64_t)kg * p.cmax + c) * MG + cg;
+    float* po = p.part_o + slot * D + 4 * grp;
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i) *(f32x4*)(po + 16 * i) = acc[i];
+    if (grp == 0) p.part_ml[slot] = make_float2(m_run, l_tot);
+  }
+}
+
+// Merge, one workgroup per (sequence, KV head); thread = (head, 4 dims).
+__global__ __launch_bounds__(512) void merge_kernel(GroupedParams p) {
+  const int b = blockIdx.x / p.num_kv_heads, g = blockIdx.x - b * p.num_kv_heads;
+  const int G = p.group, D = p.head_dim, MG = p.group_size * G;
+  const int h = threadIdx.x / (D / 4), d4 = threadIdx.x - h * (D / 4);
+  if (h >= G) return;
+  const int k = b / p.group_size, m = b - k * p.group_size;
+  const int64_t row = (int64_t)b * p.num_q_heads + (int64_t)g * G + h;
+  // the suffix row (normalised) as a piece of weight 2^lse
+  float M = p.lse[row];
+  float S = M > -__builtin_inff() ? 1.f : 0.f;
+  f32x4 acc = *(const f32x4*)(p.out32 + row * D + 4 * d4);
+  const int Sk = p.group_shared[k], chunk = prefix_chunk(Sk, p);
+  const int chunks = (Sk + chunk - 1) / chunk;
+  const int64_t item0 = ((int64_t)k * p.num_kv_heads + g) * p.cmax;
+  constexpr int BATCH = 4;  // partials loaded per batch, all loads first
+  for (int c0 = 0; c0 < chunks; c0 += BATCH) {
+    float2 ml[BATCH];
+    f32x4 o[BATCH];
+#pragma unroll
+    for (int i = 0; i < BATCH; ++i) {
+      ml[i] = make_float2(-__builtin_inff(), 0.f);
+      o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (c0 + i < chunks) {
+        const int64_t slot = (item0 + c0 + i) * MG + m * G + h;
+        ml[i] = p.part_ml[slot];
+        o[i] = *(const f32x4*)(p.part_o + slot * D + 4 * d4);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < BATCH; ++i) {
+      if (ml[i].x > M) {
+        const float sc = __builtin_amdgcn_exp2f(M - ml[i].x);
+        acc = acc * sc + o[i];
+        S = S * sc + ml[i].y;
+        M = ml[i].x;
+      } else if (ml[i].x > -__builtin_inff()) {
+        const float w = __builtin_amdgcn_exp2f(ml[i].x - M);
+        acc += w * o[i];
+        S += w * ml[i].y;
+      }
+    }
+  }
+  const float inv = S > 0.f ? 1.f / S : 0.f;
+  *(bf16x4*)(p.out + row * D + 4 * d4) = bf16x4{(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv),
+                                              (__bf16)(acc[2] * inv), (__bf16)(acc[3] * inv)};
+}
+
+template <int D, int P, bool FP8>
+static const void* prefix_fn() {
+  return (const void*)&prefix_kernel<D, P, FP8>;
+}
+
+hipError_t launch_grouped_prefix(const GroupedParams& p, int grid, bool fp8, hipStream_t s) {
+  if (grid <= 0) return hipSuccess;
+  const void* fn;
+  if (p.head_dim == 128)
+    fn = p.page_size == 16 ? (fp8 ? prefix_fn<128, 16, true>() : prefix_fn<128, 16, false>())
+                           : (fp8 ? prefix_fn<128, 32, true>() : prefix_fn<128, 32, false>());
+  else
+    fn = p.page_size == 16 ? (fp8 ? prefix_fn<64, 16, true>() : prefix_fn<64, 16, false>())
+                           : (fp8 ? prefix_fn<64, 32, true>() : prefix_fn<64, 32, false>());
+  GroupedParams arg = p;
+  void* args[] = {(void*)&arg};
+  return hipLaunchKernel(fn, dim3((unsigned)grid), dim3(kPrefixThreads), args, 0, s);
+}
+
+hipError_t launch_grouped_merge(const GroupedParams& p, hipStream_t s) {
+  hipLaunchKernelGGL(merge_kernel, dim3(p.num_seqs * p.num_kv_heads),
+                     dim3(p.group * (p.head_dim / 4)), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace dora

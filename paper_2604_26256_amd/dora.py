@@ -75,6 +75,11 @@ _lib.dora_decode_workspace_bytes.argtypes = [_DescP]
 _lib.dora_decode_workspace_bytes.restype = _SZ
 _lib.dora_decode_attn.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
 _lib.dora_decode_attn.restype = ctypes.c_int
+_lib.dora_decode_grouped_workspace_bytes.argtypes = [_DescP, _I32]
+_lib.dora_decode_grouped_workspace_bytes.restype = _SZ
+_lib.dora_decode_attn_grouped.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _I32, _P, _P,
+                                          _SZ, _P]
+_lib.dora_decode_attn_grouped.restype = ctypes.c_int
 _lib.dora_kv_append.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
 _lib.dora_kv_append.restype = ctypes.c_int
 _lib.dora_plan_partition.argtypes = [ctypes.POINTER(_I64), _I32, _I32, ctypes.POINTER(_I32)]
@@ -219,6 +224,11 @@ def dora_decode_workspace_bytes(desc: dora_decode_desc) -> int:
     return int(_lib.dora_decode_workspace_bytes(ctypes.byref(desc)))
 
 
+def dora_decode_grouped_workspace_bytes(desc: dora_decode_desc, group_size) -> int:
+    """Workspace of dora_decode_attn_grouped (0 on invalid arguments)."""
+    return int(_lib.dora_decode_grouped_workspace_bytes(ctypes.byref(desc), int(group_size)))
+
+
 _ws_cache = {}
 
 
@@ -289,6 +299,65 @@ def dora_decode_attn(q, k_pages, v_pages, block_table, seq_lens, version_ids, ou
                                _stream_handle(stream))
     del arr
     _check(st, "dora_decode_attn")
+    return out
+
+
+_gws_cache = {}
+
+
+def dora_decode_attn_grouped(q, k_pages, v_pages, block_table, seq_lens, version_ids, out, *,
+                             group_size, num_kv_heads, page_size, kv_dtype=DORA_KV_BF16,
+                             sm_scale=0.0, k_scales=None, v_scales=None, page_owner=None,
+                             flags=0, shared_pages_out=None, workspace=None, stream=None):
+    """Decode attention for groups of `group_size` consecutive sequences; the
+    pages a group's members share (same leading page ids, full pages) are read
+    once per group.  shared_pages_out: optional device int32 [B / group_size]
+    that receives each group's shared page count.  See include/dora.h."""
+    torch = _torch()
+    B, Hq, D = (int(x) for x in q.shape)
+    num_pages, kv_types = _kv_geometry(k_pages, v_pages, num_kv_heads, page_size, D, kv_dtype)
+    if block_table.dim() != 2 or block_table.shape[0] != B:
+        raise ValueError("block_table must be [B][stride]")
+    stride = int(block_table.shape[1])
+    desc = make_decode_desc(num_seqs=B, num_q_heads=Hq, num_kv_heads=num_kv_heads, head_dim=D,
+                            page_size=page_size, block_table_stride=max(1, stride),
+                            num_pages=num_pages, kv_dtype=kv_dtype, sm_scale=sm_scale,
+                            k_scales=k_scales, v_scales=v_scales, page_owner=page_owner,
+                            flags=flags)
+    if B == 0:
+        return out
+    M = int(group_size)
+    args = [
+        _dev_ptr(q, "q", (torch.bfloat16,), shape=(B, Hq, D)),
+        _dev_ptr(k_pages, "k_pages", kv_types),
+        _dev_ptr(v_pages, "v_pages", kv_types),
+        _dev_ptr(block_table, "block_table", (torch.int32,), shape=(B, stride), align=4),
+        _dev_ptr(seq_lens, "seq_lens", (torch.int32,), shape=(B,), align=4),
+        _opt_ptr(version_ids, "version_ids", (torch.int32,), shape=(B,), align=4),
+        _dev_ptr(out, "out", (torch.bfloat16,), shape=(B, Hq, D)),
+        M,
+        _opt_ptr(shared_pages_out, "shared_pages_out", (torch.int32,),
+                 shape=(B // M if M > 0 else 0,), align=4),
+    ]
+    if kv_dtype == DORA_KV_FP8_E4M3:
+        _dev_ptr(k_scales, "k_scales", (torch.float32,), shape=(num_pages,), align=4)
+        _dev_ptr(v_scales, "v_scales", (torch.float32,), shape=(num_pages,), align=4)
+    need = int(_lib.dora_decode_grouped_workspace_bytes(ctypes.byref(desc), M))
+    if need == 0:  # invalid arguments: the call reports which status
+        _check(_lib.dora_decode_attn_grouped(ctypes.byref(desc), *args, None, 0,
+                                             _stream_handle(stream)),
+               "dora_decode_attn_grouped")
+    if workspace is None:
+        key = (q.device.index, need)
+        workspace = _gws_cache.get(key)
+        if workspace is None:
+            _gws_cache.clear()
+            workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+            _gws_cache[key] = workspace
+    st = _lib.dora_decode_attn_grouped(ctypes.byref(desc), *args,
+                                       _dev_ptr(workspace, "workspace", (torch.uint8,)),
+                                       workspace.numel(), _stream_handle(stream))
+    _check(st, "dora_decode_attn_grouped")
     return out
 
 

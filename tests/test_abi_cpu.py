@@ -100,6 +100,34 @@ def test_decode_host_validation(d):
                                         None) == d.DORA_ERR_INVALID_ARG
 
 
+def test_grouped_host_validation_and_workspace(d):
+    lib = d.library()
+    P = ctypes.c_void_p
+    desc = _desc(d, num_seqs=8, num_q_heads=28, num_kv_heads=4)          # G = 7
+    base = lib.dora_decode_grouped_workspace_bytes(ctypes.byref(desc), 4)
+    assert base > d.dora_decode_workspace_bytes(desc)
+    assert d.dora_decode_grouped_workspace_bytes(desc, 4) == base
+    assert lib.dora_decode_grouped_workspace_bytes(ctypes.byref(desc), 3) == 0     # 8 % 3
+    assert lib.dora_decode_grouped_workspace_bytes(ctypes.byref(desc), 0) == 0
+    big = _desc(d, num_seqs=32, num_q_heads=28, num_kv_heads=4)
+    assert lib.dora_decode_grouped_workspace_bytes(ctypes.byref(big), 32) == 0     # 32*7 cols
+
+    def call(desc, M, **kw):
+        a = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, out=FAKE, ws=FAKE)
+        a.update(kw)
+        return lib.dora_decode_attn_grouped(ctypes.byref(desc), P(a["q"]), P(a["k"]), P(a["v"]),
+                                            P(a["bt"]), P(a["lens"]), None, P(a["out"]), M,
+                                            None, P(a["ws"]), a.get("ws_bytes", 1 << 40), None)
+
+    assert call(desc, 0) == d.DORA_ERR_INVALID_ARG
+    assert call(desc, 3) == d.DORA_ERR_INVALID_ARG
+    assert call(big, 32) == d.DORA_ERR_UNSUPPORTED
+    assert call(desc, 4, q=0) == d.DORA_ERR_INVALID_ARG
+    assert call(desc, 4, out=FAKE + 2) == d.DORA_ERR_INVALID_ARG
+    assert call(desc, 4, ws_bytes=base - 1) == d.DORA_ERR_WORKSPACE_TOO_SMALL
+    assert call(_desc(d, num_seqs=0), 4) == d.DORA_OK
+
+
 def test_append_host_validation(d):
     P = ctypes.c_void_p
     lib = d.library()

@@ -261,6 +261,23 @@ def test_physical_page_permutation_is_bitwise_invariant():
     assert np.array_equal(got, ref)
 
 
+def test_pages_shared_between_sequences_equal_private_copies():
+    """Block tables of several sequences naming the same leading pages (a shared
+    prompt) decode exactly as if each sequence held its own copy."""
+    pb = Problem([40, 33, 50, 64], 8, 2, 64, 16, 0, seed=33)
+    shared = 2                                      # pages 0 and 1 of sequence 0
+    bt = pb.bt.copy()
+    for s in (1, 2, 3):
+        bt[s, :shared] = pb.bt[0, :shared]          # point at sequence 0's pages
+    got_shared = oracle.decode(pb.q, pb.kp, pb.vp, bt, pb.lens, num_kv_heads=2, page_size=16)
+    kp2, vp2 = pb.kp.copy(), pb.vp.copy()
+    for s in (1, 2, 3):                             # private copies of sequence 0's pages
+        kp2[pb.bt[s, :shared]] = pb.kp[pb.bt[0, :shared]]
+        vp2[pb.bt[s, :shared]] = pb.vp[pb.bt[0, :shared]]
+    got_copies = oracle.decode(pb.q, kp2, vp2, pb.bt, pb.lens, num_kv_heads=2, page_size=16)
+    assert np.array_equal(got_shared, got_copies)
+
+
 def test_tail_slots_never_read():
     a = Problem([17, 3, 31], 8, 2, 64, 16, 0, seed=41, poison=True)
     b = Problem([17, 3, 31], 8, 2, 64, 16, 0, seed=41, poison=False)

@@ -318,6 +318,60 @@ def make_batch(w: Workload, device="cpu", seed_index: Optional[int] = None,
         page_owner=torch.from_numpy(owner).to(device))
 
 
+# A GRPO-shaped rollout batch: responses of one prompt share the prompt's full
+# pages (16 responses per prompt as in the paper's setup, App. B); response
+# lengths follow the 7B-class long-tail law; prompts are 1-4k tokens.
+GRPO_WORKLOAD = Workload("grpo7b", 64, 28, 4, 128, 16, 0, 32768, "lognormal", 2048, 1.2, 64,
+                         32768)
+GRPO_GROUP = 16
+GRPO_PROMPT = (1024, 4096)
+
+
+def make_grpo_batch(w: Workload = GRPO_WORKLOAD, group_size: int = GRPO_GROUP,
+                    prompt_range=GRPO_PROMPT, device="cpu", seed_index: int = 5,
+                    poison: bool = True):
+    """Batch whose sequences come in groups of `group_size` responses to one
+    prompt: every member's block table starts with the same page ids for the
+    prompt's full pages (the partial last prompt page is private, as in a
+    copy-on-write pool).  Returns (batch, shared_pages int32 [B])."""
+    import torch
+
+    sd = seeds(seed_index)
+    rng = np.random.default_rng(sd[6])
+    n_groups = w.num_seqs // group_size
+    assert n_groups * group_size == w.num_seqs
+    prompt = rng.integers(prompt_range[0], prompt_range[1] + 1, n_groups)
+    lengths = (np.repeat(prompt, group_size) + sample_lengths(w, sd[0])).astype(np.int32)
+    b = make_batch(w, device=device, seed_index=seed_index, lengths=lengths, poison=poison)
+    shared = np.repeat(prompt // w.page_size, group_size).astype(np.int32)
+    bt = b.block_table_h.copy()
+    for g in range(n_groups):
+        lead = g * group_size
+        for m in range(lead + 1, lead + group_size):
+            bt[m, :shared[m]] = bt[lead, :shared[m]]
+    n = pages_needed(lengths, w.page_size)
+    b.block_table_h = bt
+    b.block_table = torch.from_numpy(bt).to(device)
+    b.used_pages = np.unique(np.concatenate([bt[i, :n[i]] for i in range(w.num_seqs)]))
+    return b, shared
+
+
+def shared_prefix_algorithmic_bytes(w: Workload, lengths: np.ndarray, shared: np.ndarray,
+                                    group_size: int) -> dict:
+    """algorithmic_bytes with each shared page's K and V counted once per group
+    (block-table entries are still read per sequence)."""
+    ab = algorithmic_bytes(w, lengths)
+    shared = np.asarray(shared, np.int64)
+    members = np.arange(len(shared)) % group_size != 0          # all but the group leader
+    dup = int(shared[members].sum()) * w.page_size * w.num_kv_heads * w.head_dim * 2 * \
+        w.elem_bytes
+    ab = dict(ab)
+    ab["kv"] -= dup
+    ab["total"] -= dup
+    ab["shared_kv_counted_once"] = dup
+    return ab
+
+
 def subset_for_oracle(batch: Batch, seqs: Sequence[int]) -> dict:
     """Host copies of the inputs of a few sequences, with their pages renumbered
     into a compact pool, for the oracle (which cannot hold the full pool)."""

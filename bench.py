@@ -42,12 +42,15 @@ CALIBRATION_BYTES = 2 << 30                        # read and written per dispat
 TRACE_CMD = ("cd /tmp && rocprofv3 --kernel-trace --stats --output-format csv "
              "-d $REPO/gpurun_out/prof_trace_{w} -o run -- python $REPO/bench.py --only-main "
              "--workload {w} --no-cpu-baseline --steps 30")
+GRPO_TRACE_CMD = ("cd /tmp && rocprofv3 --kernel-trace --stats --output-format csv "
+                  "-d $REPO/gpurun_out/prof_trace_grpo7b -o run -- python $REPO/bench.py "
+                  "--grpo-only --steps 30")
 PMC_CMD = ("cd /tmp && timeout -s KILL 300 rocprofv3 --pmc {c} --output-format csv "
            "-d $REPO/gpurun_out/pmc_{d}_{w} -o run -- python $REPO/bench.py --only-main "
            "--workload {w} --no-cpu-baseline --steps 5 --warmup 1")
 L2_COUNTERS = "TCC_HIT_sum TCC_MISS_sum"
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2604_26256_amd", "csrc", f)
-                  for f in ("decode.hip", "dora_internal.h", "api.cpp")]
+                  for f in ("decode.hip", "decode_core.h", "dora_internal.h", "api.cpp")]
 
 
 def kernel_source_hash() -> str:
@@ -75,6 +78,10 @@ def parse():
                     help="evict caches by reading (clean lines) or writing 1 GiB")
     ap.add_argument("--num-waves", type=int, default=0,
                     help="decode wavefronts (0 = one per resident slot)")
+    ap.add_argument("--grpo-only", action="store_true",
+                    help="time only the GRPO batch (plain against grouped decode)")
+    ap.add_argument("--summarize-grpo-trace", metavar="DIR",
+                    help="write the kernel-trace summary of a --grpo-only rocprofv3 run")
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="write the kernel-trace summary of a rocprofv3 run under profiles/")
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "L2_DIR"),
@@ -99,15 +106,24 @@ def pmc_path(workload):
     return os.path.join(PROFILES, f"decode_kernel_{workload}_pmc.json")
 
 
-def summarize_trace(d, workload):
+def summarize_trace(d, workload, grpo=False):
     import csv
     rows = list(csv.DictReader(open(_find_csv(d, "kernel_stats.csv"))))
-    out = os.path.join(PROFILES, f"decode_kernel_{workload}_trace.md")
-    lines = [f"# rocprofv3 kernel trace: {workload}", "",
-             "Command (repo root as $REPO):", "", "    " + TRACE_CMD.format(w=workload), "",
-             "Per-kernel durations from `run_kernel_stats.csv` (all dispatches of the run:",
-             "warm-up, timed steps and the per-kernel event pass).", "",
-             "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
+    if grpo:
+        out = os.path.join(PROFILES, "grouped_decode_grpo7b_trace.md")
+        head = ["# rocprofv3 kernel trace: GRPO batch, plain and grouped decode", "",
+                "Command (repo root as $REPO):", "", "    " + GRPO_TRACE_CMD, "",
+                "`decode_kernel<..., false>` is the plain path; the grouped call runs",
+                "`prefix_kernel`, `decode_kernel<..., true>` (the suffix), the combine",
+                "kernel and `merge_kernel`.  Per-kernel durations from",
+                "`run_kernel_stats.csv` (all dispatches: warm-up and timed calls).", ""]
+    else:
+        out = os.path.join(PROFILES, f"decode_kernel_{workload}_trace.md")
+        head = [f"# rocprofv3 kernel trace: {workload}", "",
+                "Command (repo root as $REPO):", "", "    " + TRACE_CMD.format(w=workload), "",
+                "Per-kernel durations from `run_kernel_stats.csv` (all dispatches of the run:",
+                "warm-up, timed steps and the per-kernel event pass).", ""]
+    lines = head + ["| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
     for r in rows:
         name = r.get("Name") or r.get("KernelName") or ""
         if not any(k in name for k in ("dora::", "reduce_kernel", CALIBRATION_KERNEL)):
@@ -138,17 +154,19 @@ def summarize_pmc(fetch_dir, write_dir, l2_dir, workload):
     hit = per_kernel(l2_dir, "TCC_HIT_sum")
     miss = per_kernel(l2_dir, "TCC_MISS_sum")
 
-    def pick(acc, key, largest_grid=False):
+    def pick(acc, key, calibration=False):
         vals = [v for k, lst in acc.items() if key in k for v in lst]
         if not vals:
             raise ValueError(f"no dispatches of {key} in the counter data")
-        if largest_grid:
-            g = max(v[0] for v in vals)
-            vals = [v for v in vals if v[0] == g]
+        if calibration:
+            # the 2 GiB copy: the largest copy of the run (other copies, such as
+            # the pack set's, share its grid but move less)
+            top = max(v[1] for v in vals)
+            vals = [v for v in vals if v[1] >= 0.5 * top]
         return sum(v[1] for v in vals) / len(vals), len(vals)
 
-    cf, ncf = pick(fetch, CALIBRATION_KERNEL, largest_grid=True)
-    cw, ncw = pick(write, CALIBRATION_KERNEL, largest_grid=True)
+    cf, ncf = pick(fetch, CALIBRATION_KERNEL, calibration=True)
+    cw, ncw = pick(write, CALIBRATION_KERNEL, calibration=True)
     ff = CALIBRATION_BYTES / (cf * 1024)
     fw = CALIBRATION_BYTES / (cw * 1024)
     df, ndf = pick(fetch, DECODE_KERNEL)
@@ -481,7 +499,9 @@ def load_pmc(w):
 
 def main():
     args = parse()
-    if args.summarize_trace or args.summarize_pmc:
+    if args.summarize_trace or args.summarize_pmc or args.summarize_grpo_trace:
+        if args.summarize_grpo_trace:
+            summarize_trace(args.summarize_grpo_trace, None, grpo=True)
         if args.summarize_trace:
             summarize_trace(args.summarize_trace, args.workload)
         if args.summarize_pmc:
@@ -510,6 +530,9 @@ def main():
     else:
         flush = lambda: flush_buf.fill_(1.0)  # noqa: E731
 
+    if args.grpo_only:
+        print(json.dumps(time_grpo(torch, dora, args.steps, flush), indent=1))
+        return
     names = [args.workload] + ([] if args.only_main else
                                [w.name for w in wl.WORKLOADS if w.name != args.workload])
     results, main_rec, main_t, main_batch = {}, None, None, None

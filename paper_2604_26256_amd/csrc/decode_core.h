@@ -80,23 +80,28 @@ __device__ __forceinline__ void load_page(PageRegs<D, P, FP8>& r, const uint8_t*
 
 // One page of one segment: scores S^T = K Q^T for the 16 query columns of the
 // lane layout, online-softmax update in the log2 domain, then O^T += V^T P^T.
-// `r` holds the page as each lane loaded it (from HBM or LDS); nvalid tokens
-// of the page count; ksc folds the softmax scale (and the fp8 K page scale),
-// vsc the fp8 V page scale.  Shared by the decode and the group-prefix kernel.
-template <int D, int P, bool FP8>
-__device__ __forceinline__ void consume_page(const PageRegs<D, P, FP8>& r, int nvalid, float ksc,
-                                             float vsc, const bf16x8 (&qop)[D / 32],
-                                             f32x4 (&acc)[D / 16], float& m_run, float& l_run) {
+// NC column tiles of 16 share the page's operands (each K and V register
+// feeds NC MFMAs); tile c has its own query operand, accumulator and running
+// max / sum.  `r` holds the page as each lane loaded it (from HBM or LDS);
+// nvalid tokens of the page count; ksc folds the softmax scale (and the fp8 K
+// page scale), vsc the fp8 V page scale.
+template <int D, int P, bool FP8, int NC>
+__device__ __forceinline__ void consume_page_tiles(const PageRegs<D, P, FP8>& r, int nvalid,
+                                                   float ksc, float vsc,
+                                                   const bf16x8 (&qop)[NC][D / 32],
+                                                   f32x4 (&acc)[NC][D / 16], float (&m_run)[NC],
+                                                   float (&l_run)[NC]) {
   constexpr int NT = PageRegs<D, P, FP8>::NT;
   constexpr int KSTEPS = D / 32;
   constexpr int DBLK = D / 16;
   const int grp = (threadIdx.x & 63) >> 4;
 
   // scores S^T: lane holds tokens of its row group for head `col`
-  f32x4 sc[NT];
+  f32x4 sc[NC][NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NC; ++c) sc[c][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
       bf16x8 a;
@@ -106,44 +111,52 @@ __device__ __forceinline__ void consume_page(const PageRegs<D, P, FP8>& r, int n
       } else {
         a = __builtin_bit_cast(bf16x8, r.k[t * KSTEPS + ks]);
       }
-      s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[ks], s, 0, 0, 0);
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        sc[c][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[c][ks], sc[c][t], 0, 0, 0);
     }
-    sc[t] = s;
   }
-  float mx = -__builtin_inff();
+  float alpha[NC];
 #pragma unroll
-  for (int t = 0; t < NT; ++t)
+  for (int c = 0; c < NC; ++c) {
+    float mx = -__builtin_inff();
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float x = sc[t][i] * ksc;
-      const int tok = P == 16 ? 4 * grp + i : 8 * grp + 4 * t + i;
-      if (nvalid < P && tok >= nvalid) x = -__builtin_inff();
-      sc[t][i] = x;
-      mx = fmaxf(mx, x);
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float x = sc[c][t][i] * ksc;
+        const int tok = P == 16 ? 4 * grp + i : 8 * grp + 4 * t + i;
+        if (nvalid < P && tok >= nvalid) x = -__builtin_inff();
+        sc[c][t][i] = x;
+        mx = fmaxf(mx, x);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run[c], mx);
+    alpha[c] = __builtin_amdgcn_exp2f(m_run[c] - m_new);
+    m_run[c] = m_new;
+    float psum = 0.f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float e = __builtin_amdgcn_exp2f(sc[c][t][i] - m_new);
+        psum += e;
+        sc[c][t][i] = e * vsc;
+      }
+    l_run[c] = l_run[c] * alpha[c] + psum;
+    if (__ballot(alpha[c] != 1.f)) {
+#pragma unroll
+      for (int i = 0; i < DBLK; ++i) acc[c][i] *= alpha[c];
     }
-  mx = fmaxf(mx, __shfl_xor(mx, 16));
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const float m_new = fmaxf(m_run, mx);
-  const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-  m_run = m_new;
-  float psum = 0.f;
-#pragma unroll
-  for (int t = 0; t < NT; ++t)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float e = __builtin_amdgcn_exp2f(sc[t][i] - m_new);
-      psum += e;
-      sc[t][i] = e * vsc;
-    }
-  l_run = l_run * alpha + psum;
-  if (__ballot(alpha != 1.f)) {
-#pragma unroll
-    for (int i = 0; i < DBLK; ++i) acc[i] *= alpha;
   }
   // P^T operand, then O^T += V^T P^T per 16-row block of the head dim
   if constexpr (P == 16) {
-    const bf16x4 pb4 = bf16x4{(__bf16)sc[0][0], (__bf16)sc[0][1], (__bf16)sc[0][2],
-                              (__bf16)sc[0][3]};
+    bf16x4 pb4[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+      pb4[c] = bf16x4{(__bf16)sc[c][0][0], (__bf16)sc[c][0][1], (__bf16)sc[c][0][2],
+                      (__bf16)sc[c][0][3]};
 #pragma unroll
     for (int i = 0; i < DBLK; ++i) {
       bf16x4 a;
@@ -156,12 +169,17 @@ __device__ __forceinline__ void consume_page(const PageRegs<D, P, FP8>& r, int n
         for (int e = 0; e < 4; ++e)
           if (4 * grp + e >= nvalid) a[e] = (__bf16)0.f;
       }
-      acc[i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, pb4, acc[i], 0, 0, 0);
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, pb4[c], acc[c][i], 0, 0, 0);
     }
   } else {
-    const bf16x8 pb8 = bf16x8{(__bf16)sc[0][0], (__bf16)sc[0][1], (__bf16)sc[0][2],
-                              (__bf16)sc[0][3], (__bf16)sc[1][0], (__bf16)sc[1][1],
-                              (__bf16)sc[1][2], (__bf16)sc[1][3]};
+    bf16x8 pb8[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+      pb8[c] = bf16x8{(__bf16)sc[c][0][0], (__bf16)sc[c][0][1], (__bf16)sc[c][0][2],
+                      (__bf16)sc[c][0][3], (__bf16)sc[c][1][0], (__bf16)sc[c][1][1],
+                      (__bf16)sc[c][1][2], (__bf16)sc[c][1][3]};
 #pragma unroll
     for (int i = 0; i < DBLK; ++i) {
       bf16x8 a;
@@ -174,9 +192,23 @@ __device__ __forceinline__ void consume_page(const PageRegs<D, P, FP8>& r, int n
         for (int e = 0; e < 8; ++e)
           if (8 * grp + e >= nvalid) a[e] = (__bf16)0.f;
       }
-      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb8, acc[i], 0, 0, 0);
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        acc[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb8[c], acc[c][i], 0, 0, 0);
     }
   }
+}
+
+// The step for one column tile (the decode kernel's case).
+template <int D, int P, bool FP8>
+__device__ __forceinline__ void consume_page(const PageRegs<D, P, FP8>& r, int nvalid, float ksc,
+                                             float vsc, const bf16x8 (&qop)[D / 32],
+                                             f32x4 (&acc)[D / 16], float& m_run, float& l_run) {
+  consume_page_tiles<D, P, FP8, 1>(r, nvalid, ksc, vsc,
+                                   reinterpret_cast<const bf16x8(&)[1][D / 32]>(qop),
+                                   reinterpret_cast<f32x4(&)[1][D / 16]>(acc),
+                                   reinterpret_cast<float(&)[1]>(m_run),
+                                   reinterpret_cast<float(&)[1]>(l_run));
 }
 
 // Query operand: lane supplies q[row][8 head-dim values] per k-step, in the

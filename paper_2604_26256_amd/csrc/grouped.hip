@@ -9,10 +9,10 @@
 //            pages).  It finds the group's shared prefix S (leading page ids
 //            equal in every member's row, full pages of every member), then
 //            its waves stage the pages' K and V tiles in LDS (double-buffered,
-//            one barrier per step); wave t applies them to 16 of the group's
-//            (member, query head) columns with the same MFMA/online-softmax
-//            step as the decode kernel, and writes an unnormalised partial
-//            (o, running max, sum) per column.
+//            one barrier per step); each computing wave applies them to a tile
+//            of 16 of the group's (member, query head) columns with the decode
+//            kernel's MFMA/online-softmax step, and writes an unnormalised
+//            partial (o, running max, sum) per column.
 //   suffix   the decode kernel over each member's pages past S, writing fp32
 //            rows and their log-sum-exp.
 //   merge    per (sequence, KV head): the chunk partials of its prefix and its
@@ -27,6 +27,7 @@ namespace dora {
 
 constexpr int kPrefixThreads = 64 * kPrefixMaxWaves;
 constexpr int kStageSets = 2;  // steps in flight per workgroup (register staging)
+constexpr int NCW = 1;         // column tiles per computing wave (2 measured no faster)
 
 // Shared prefix of group k (all threads of the workgroup get it): the number
 // of leading pages that every member holds in full (floor(len / P), at most
@@ -38,21 +39,25 @@ __device__ int shared_prefix(const GroupedParams& p, int k, int enough) {
   const int M = p.group_size, P = p.page_size, stride = p.stride;
   const int64_t b0 = (int64_t)k * M;
   if (M == 1) return 0;
+  int L = 0;  // issued before the first barrier: its latency overlaps the waves' start
+  if ((int)threadIdx.x < M) L = p.seq_lens[b0 + threadIdx.x];
   if (threadIdx.x == 0) s_cap = s_min = stride;
   __syncthreads();
-  if ((int)threadIdx.x < M) {
-    const int L = p.seq_lens[b0 + threadIdx.x];
-    atomicMin(&s_cap, L > 0 ? L / P : 0);
-  }
+  if ((int)threadIdx.x < M) atomicMin(&s_cap, L > 0 ? L / P : 0);
   __syncthreads();
   const int cap = s_cap;  // final here; mismatches go to s_min
   if (cap <= enough) return cap;
-  const int32_t* __restrict__ lead = p.block_table + b0 * stride;
-  int first = cap;  // this thread's smallest mismatch; no atomics inside the
-#pragma unroll 4  // loop, so its loads issue back to back
-  for (int x = threadIdx.x; x < (M - 1) * cap; x += blockDim.x) {
-    const int m = 1 + x / cap, j = x - (m - 1) * cap;
-    if (p.block_table[(b0 + m) * stride + j] != lead[j]) first = j < first ? j : first;
+  // Thread j holds the leader's entry j and compares it with every member's;
+  // the member loads are independent, so they issue back to back (no
+  // division, no atomics inside the loops).
+  const int32_t* __restrict__ bt = p.block_table + b0 * stride;
+  int first = cap;  // this thread's smallest mismatch
+  for (int j = threadIdx.x; j < cap; j += blockDim.x) {
+    const int32_t lead = bt[j];
+    bool diff = false;
+#pragma unroll 8
+    for (int m = 1; m < M; ++m) diff |= bt[(int64_t)m * stride + j] != lead;
+    if (diff && j < first) first = j;
   }
   if (first < cap) atomicMin(&s_min, first);
   __syncthreads();
@@ -105,14 +110,18 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(GroupedParams p)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
   const int G = p.group, MG = p.group_size * G;
-  const bool computes = wave * 16 < MG;  // waves past the columns only help staging
-  const int cg = wave * 16 + col;        // this lane's column among (member, head) pairs
-  const bool active = cg < MG;
-  const int m = active ? cg / G : 0, h = active ? cg - m * G : 0;
-  const int64_t b = (int64_t)k * p.group_size + m;
-
-  bf16x8 qop[D / 32];  // issued first: it does not depend on the prefix
-  load_q_operand<D, FP8>(qop, p.q + (b * p.num_q_heads + (int64_t)g * G + h) * D, active);
+  // A computing wave takes NCW tiles of 16 (member, query head) columns (each
+  // K and V operand read from LDS then feeds NCW MFMAs).  Waves past the
+  // columns only stage.
+  const bool computes = wave * 16 * NCW < MG;
+  bf16x8 qop[NCW][D / 32];  // issued first: it does not depend on the prefix
+#pragma unroll
+  for (int t = 0; t < NCW; ++t) {
+    const int cg = (wave * NCW + t) * 16 + col;  // column among (member, head) pairs
+    const int m = cg < MG ? cg / G : 0, h = cg < MG ? cg - m * G : 0;
+    const int64_t b = (int64_t)k * p.group_size + m;
+    load_q_operand<D, FP8>(qop[t], p.q + (b * p.num_q_heads + (int64_t)g * G + h) * D, cg < MG);
+  }
 
   // The group's shared prefix; the first workgroup of each group publishes it
   // for the suffix decode and the merge.  A chunk that starts past every
@@ -128,10 +137,15 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(GroupedParams p)
   const int j1 = j0 + chunk < S ? j0 + chunk : S;
   // The item's page ids (and fp8 scales) go to LDS first: a page load that
   // waited on a block-table load would wait on every load issued before it.
-  f32x4 acc[D / 16];
+  f32x4 acc[NCW][D / 16];
+  float m_run[NCW], l_run[NCW];
 #pragma unroll
-  for (int i = 0; i < D / 16; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -__builtin_inff(), l_run = 0.f;
+  for (int t = 0; t < NCW; ++t) {
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i) acc[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m_run[t] = -__builtin_inff();
+    l_run[t] = 0.f;
+  }
 
   const int32_t* bt = p.block_table + (int64_t)k * p.group_size * p.stride;  // the leader's row
   for (int t = threadIdx.x; t < j1 - j0; t += kPrefixThreads) {
@@ -218,7 +232,7 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(GroupedParams p)
             vsc = s_vsc[jj - j0];
           }
           const int nvalid = (j1 - jj < PAIR ? j1 - jj : PAIR) * P;  // shared pages are full
-          consume_page<D, VP, FP8>(pr, nvalid, ksc, vsc, qop, acc, m_run, l_run);
+          consume_page_tiles<D, VP, FP8, NCW>(pr, nvalid, ksc, vsc, qop, acc, m_run, l_run);
         }
         if (u + 1 < n_steps) put(st[(r + 1) % kStageSets], (u + 1) & 1, u + 1);
         __syncthreads();
@@ -226,14 +240,18 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(GroupedParams p)
     }
   }
 
-  float l_tot = l_run + __shfl_xor(l_run, 16);
-  l_tot += __shfl_xor(l_tot, 32);
-  if (active) {
-    const int64_t slot = ((int64_t)kg * p.cmax + c) * MG + cg;
-    float* po = p.part_o + slot * D + 4 * grp;
 #pragma unroll
-    for (int i = 0; i < D / 16; ++i) *(f32x4*)(po + 16 * i) = acc[i];
-    if (grp == 0) p.part_ml[slot] = make_float2(m_run, l_tot);
+  for (int t = 0; t < NCW; ++t) {
+    float l_tot = l_run[t] + __shfl_xor(l_run[t], 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    const int cg = (wave * NCW + t) * 16 + col;
+    if (cg < MG) {
+      const int64_t slot = ((int64_t)kg * p.cmax + c) * MG + cg;
+      float* po = p.part_o + slot * D + 4 * grp;
+#pragma unroll
+      for (int i = 0; i < D / 16; ++i) *(f32x4*)(po + 16 * i) = acc[t][i];
+      if (grp == 0) p.part_ml[slot] = make_float2(m_run[t], l_tot);
+    }
   }
 }
 

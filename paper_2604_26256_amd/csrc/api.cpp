@@ -51,20 +51,31 @@ int min_range_of(const dora_decode_desc& d) {
 
 namespace dora {
 
+// Decode wavefronts per launch.  bf16 pages take at most kBf16WavesPerCu per
+// CU: past about one wavefront per SIMD the kernel is bound by HBM, and each
+// extra wavefront only adds cuts, partials and combine work (the 7B-class
+// batch is 4-5% faster at 5 per CU than at every resident slot; the larger
+// batches are level).  fp8 pages keep every resident slot: their per-page
+// conversion work needs the occupancy.  Never more than the batch can use:
+// at most B * Hkv * stride page-heads, min_range each.
 int64_t decode_waves(const dora_decode_desc& d) {
   if (d.num_waves > 0) return d.num_waves;
   int dev = 0, cus = 0, per_cu = 0;
+  const bool fp8 = d.kv_dtype == DORA_KV_FP8_E4M3;
   const int seqs = d.num_seqs < kMaxSeqsPerLaunch ? d.num_seqs : kMaxSeqsPerLaunch;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      decode_waves_per_cu(d.head_dim, d.page_size, d.kv_dtype == DORA_KV_FP8_E4M3, seqs,
-                          &per_cu) != hipSuccess ||
+      decode_waves_per_cu(d.head_dim, d.page_size, fp8, seqs, &per_cu) != hipSuccess ||
       cus <= 0 || per_cu <= 0) {
     (void)hipGetLastError();  // no device here: size for a 256-CU part at 8 waves per CU
     cus = 256;
     per_cu = 8;
   }
-  return (int64_t)cus * per_cu * kWaveFactor;
+  if (!fp8 && per_cu > kBf16WavesPerCu) per_cu = kBf16WavesPerCu;
+  const int64_t slots = (int64_t)cus * per_cu;
+  const int64_t most = (int64_t)seqs * d.num_kv_heads * d.block_table_stride;
+  const int64_t need = (most + min_range_of(d) - 1) / min_range_of(d);
+  return need < slots ? (need > 0 ? need : 1) : slots;
 }
 
 bool ws_layout(const dora_decode_desc& d, int64_t waves, WsLayout* out) {

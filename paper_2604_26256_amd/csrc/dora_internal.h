@@ -10,9 +10,9 @@
 
 namespace dora {
 
-// Default number of decode wavefronts per resident wavefront slot (compute
-// units x occupancy): one equal range per slot.
-constexpr int kWaveFactor = 1;
+// Decode wavefronts per compute unit for bf16 pages, at most (fp8 pages use
+// every resident slot).  One equal range per wavefront.
+constexpr int kBf16WavesPerCu = 5;
 // Smallest range (page-heads) a wavefront gets by default: a range must carry
 // enough bytes to amortise the wavefront's start-up (page prefix, first loads).
 constexpr int kMinRangePages = 8;

@@ -111,9 +111,13 @@ typedef struct {
   const int16_t* page_owner;   /* device [num_pages] owning version, or NULL; read
                                   only under DORA_FLAG_VALIDATE */
   uint32_t flags;              /* DORA_FLAG_* */
-  int32_t num_waves;           /* decode wavefronts to launch; 0 = one per
-                                  resident wavefront slot of the current device
-                                  (compute units x occupancy) */
+  int32_t num_waves;           /* decode wavefronts to launch; 0 = library
+                                  default: for fp8 pages one per resident
+                                  wavefront slot of the current device (compute
+                                  units x occupancy), for bf16 pages at most 5
+                                  per compute unit; never more than the batch
+                                  can use (B x Hkv x stride page-heads over the
+                                  minimum range) */
   int32_t min_range_pages;     /* smallest work range per wavefront, in
                                   (page, KV head) units; 0 = library default */
   void**  prof_events;         /* NULL, or 3 caller-created hipEvent_t recorded on

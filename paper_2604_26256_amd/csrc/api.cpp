@@ -5,8 +5,6 @@
 #include <stdint.h>
 #include <string.h>
 
-#include <vector>
-
 #include "dora_internal.h"
 
 using namespace dora;

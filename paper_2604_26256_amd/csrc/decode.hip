@@ -124,9 +124,15 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
     int n[8], tsum = 0;
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
+      // lanes past the batch load the last length and drop it: no branch
+      // around the load, so the eight loads issue back to back and are
+      // waited for once (a load under a branch is waited for on its own)
       const int b = base + lane * 8 + k;
-      n[k] = b < B ? pages_of(p.seq_lens[b], P, p.stride) : 0;
-      if constexpr (SUFFIX) n[k] -= b < B ? p.skip[(p.skip_seq0 + b) / p.skip_group] : 0;
+      const int bc = b < B ? b : B - 1;
+      const int L = p.seq_lens[bc];
+      int n_b = pages_of(L, P, p.stride);
+      if constexpr (SUFFIX) n_b -= p.skip[(p.skip_seq0 + bc) / p.skip_group];
+      n[k] = b < B ? n_b : 0;
       tsum += n[k];
     }
     const int incl = wave_inclusive_scan(tsum);

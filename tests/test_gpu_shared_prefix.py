@@ -100,3 +100,32 @@ def test_grouped_full_size_grpo_batch_sampled():
     assert (out.float() - run_decode(b).float()).abs().max().item() <= TOL[0]
     seqs = sorted(set([0, 1, 17, 63] + sample_seqs(b.lengths, 2, seed=5)))
     assert max_abs_err(out, oracle_for(b, seqs), seqs) <= TOL[0]
+
+
+def test_grouped_batch_larger_than_one_launch():
+    """9,000 sequences in groups of 8: the suffix decode is cut into launches of
+    8,192 sequences, and a group (1,024) straddles the cut; sequences on both
+    sides match the oracle and the plain path."""
+    w = wl.Workload("big", 9000, 8, 2, 64, 16, 0, 131072, "lognormal", 20, 1.0, 1, 60)
+    b, shared = wl.make_grpo_batch(w, group_size=8, prompt_range=(16, 100), device="cuda",
+                                   seed_index=43)
+    out, det = _grouped(b, 8)
+    assert det.tolist() == shared[::8].tolist()
+    assert (out.float() - run_decode(b).float()).abs().max().item() <= TOL[0]
+    seqs = sorted(set([0, 7, 8184, 8191, 8192, 8199, 8999] + sample_seqs(b.lengths, 6, seed=7)))
+    assert max_abs_err(out, oracle_for(b, seqs), seqs) <= TOL[0]
+
+
+def test_grouped_validate_flag():
+    w = wl.Workload("v", 8, 14, 2, 128, 16, 0, 4096, "lognormal", 300, 1.0, 1, 2000)
+    b, shared = wl.make_grpo_batch(w, group_size=4, prompt_range=(100, 600), device="cuda",
+                                   seed_index=44)
+    d = lib()
+    good, _ = _grouped(b, 4, flags=d.DORA_FLAG_VALIDATE, page_owner=b.page_owner)
+    assert max_abs_err(good, oracle_for(b)) <= TOL[0]
+    bt = b.block_table.clone()
+    bt[5, 0] = w.num_pages + 3                       # out of the pool
+    b.block_table = bt
+    with pytest.raises(d.DoraError) as e:
+        _grouped(b, 4, flags=d.DORA_FLAG_VALIDATE, page_owner=b.page_owner)
+    assert e.value.status == d.DORA_ERR_DEVICE_CHECK

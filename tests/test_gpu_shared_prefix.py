@@ -39,6 +39,8 @@ def _set_tables(b, bt, lens=None):
     (0, 32, 64, 1, 16),      # one query head per KV head, 16 members
     (1, 16, 128, 16, 2),     # 16 query heads per KV head: 32 columns
     (0, 16, 128, 8, 16),     # 128 columns: the widest group
+    (1, 32, 128, 8, 16),     # the widest group over fp8 pages of 32 tokens
+    (1, 16, 64, 4, 8),       # fp8, d 64
 ])
 def test_grouped_matches_oracle_and_plain_decode(dt, P, d, G, M):
     print(f"[case] grouped dt={dt} P={P} d={d} G={G} M={M}", flush=True)

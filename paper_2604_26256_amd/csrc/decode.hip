@@ -243,8 +243,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
 
   auto finish_segment = [&]() {
     // Sum of exponentials over the four row groups (same head, other tokens).
-    float l_tot = l_run + __shfl_xor(l_run, 16);
-    l_tot += __shfl_xor(l_tot, 32);
+    const float l_tot = sum_xor32(sum_xor16(l_run));
     if (col < G) {
       if (seg_whole) {
         const float inv = 1.f / l_tot;

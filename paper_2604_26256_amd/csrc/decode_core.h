@@ -22,6 +22,32 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 // decode
 // ---------------------------------------------------------------------------
 
+// Butterflies across the 16-lane rows of a wave (each lane with lane ^ 16, or
+// with lane ^ 32) on gfx950's row-swap permutes, VALU operations instead of
+// an LDS-routed shuffle.  A swap of a value with itself returns, in its two
+// results, the lane's value and its partner's (in an order that depends on
+// the row), so their max or sum is the butterfly's, bit for bit.
+__device__ __forceinline__ float max_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Raw bytes of one page's K and V tiles for one KV head, as each lane loads them.
 template <int D, int P, bool FP8>
 struct PageRegs {
@@ -130,8 +156,7 @@ __device__ __forceinline__ void consume_page_tiles(const PageRegs<D, P, FP8>& r,
         sc[c][t][i] = x;
         mx = fmaxf(mx, x);
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = max_xor32(max_xor16(mx));
     const float m_new = fmaxf(m_run[c], mx);
     alpha[c] = __builtin_amdgcn_exp2f(m_run[c] - m_new);
     m_run[c] = m_new;

@@ -242,8 +242,7 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(GroupedParams p)
 
 #pragma unroll
   for (int t = 0; t < NCW; ++t) {
-    float l_tot = l_run[t] + __shfl_xor(l_run[t], 16);
-    l_tot += __shfl_xor(l_tot, 32);
+    const float l_tot = sum_xor32(sum_xor16(l_run[t]));
     const int cg = (wave * NCW + t) * 16 + col;
     if (cg < MG) {
       const int64_t slot = ((int64_t)kg * p.cmax + c) * MG + cg;

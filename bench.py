@@ -413,25 +413,12 @@ def time_pack(torch, dora, b, steps, flush):
     packed = torch.empty(dora.dora_kv_packed_bytes(desc, npg), dtype=torch.uint8, device="cuda")
     geo = dict(num_kv_heads=w.num_kv_heads, page_size=w.page_size, head_dim=w.head_dim,
                kv_dtype=w.kv_dtype)
-    pk, up = [], []
-    for i in range(steps + 2):
-        flush()
-        s0, s1, s2 = make_events(torch, 3)
-        s0.record()
-        dora.dora_kv_page_pack(b.k_pages, b.v_pages, src_t, packed, policy_version=0,
-                               n_seqs=len(seqs), **geo)
-        s1.record()
-        flush()
-        torch.cuda.synchronize()
-        s1b = make_events(torch, 1)[0]
-        s1b.record()
-        dora.dora_kv_page_unpack(packed, dst_t, b.k_pages, b.v_pages, src_version=0,
-                                 policy_version=0, **geo)
-        s2.record()
-        torch.cuda.synchronize()
-        if i >= 2:
-            pk.append(s0.elapsed_time(s1))
-            up.append(s1b.elapsed_time(s2))
+    pk = time_calls(torch, lambda: dora.dora_kv_page_pack(
+        b.k_pages, b.v_pages, src_t, packed, policy_version=0, n_seqs=len(seqs), **geo),
+        steps, 2, flush)
+    up = time_calls(torch, lambda: dora.dora_kv_page_unpack(
+        packed, dst_t, b.k_pages, b.v_pages, src_version=0, policy_version=0, **geo),
+        steps, 2, flush)
     moved = 2 * npg * w.page_bytes          # K and V pages, one way
     rec = {"seqs": int(len(seqs)), "pages": int(npg), "bytes_one_way": int(moved),
            "pack_ms": float(np.mean(pk)), "unpack_ms": float(np.mean(up)),

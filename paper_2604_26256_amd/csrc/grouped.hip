@@ -254,7 +254,11 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(GroupedParams p)
   }
 }
 
-// Merge, one workgroup per (sequence, KV head); thread = (head, 4 dims).
+// Merge, one workgroup per (sequence, KV head); thread = (head, 4 dims).  The
+// suffix row, the group's prefix length and the first BATCH chunk partials are
+// loaded together: slots past the group's chunk count lie inside the
+// (group, KV head)'s cmax slots and are read and dropped, so the common case
+// (at most BATCH chunks) costs one round trip.
 __global__ __launch_bounds__(512) void merge_kernel(GroupedParams p) {
   const int b = blockIdx.x / p.num_kv_heads, g = blockIdx.x - b * p.num_kv_heads;
   const int G = p.group, D = p.head_dim, MG = p.group_size * G;
@@ -262,29 +266,32 @@ __global__ __launch_bounds__(512) void merge_kernel(GroupedParams p) {
   if (h >= G) return;
   const int k = b / p.group_size, m = b - k * p.group_size;
   const int64_t row = (int64_t)b * p.num_q_heads + (int64_t)g * G + h;
+  const int64_t item0 = ((int64_t)k * p.num_kv_heads + g) * p.cmax;
+  constexpr int BATCH = 16;
+  float2 ml[BATCH];
+  f32x4 o[BATCH];
+  auto load_batch = [&](int c0) {
+#pragma unroll
+    for (int i = 0; i < BATCH; ++i) {
+      const int c = c0 + i < p.cmax ? c0 + i : p.cmax - 1;
+      const int64_t slot = (item0 + c) * MG + m * G + h;
+      ml[i] = p.part_ml[slot];
+      o[i] = *(const f32x4*)(p.part_o + slot * D + 4 * d4);
+    }
+  };
   // the suffix row (normalised) as a piece of weight 2^lse
   float M = p.lse[row];
-  float S = M > -__builtin_inff() ? 1.f : 0.f;
   f32x4 acc = *(const f32x4*)(p.out32 + row * D + 4 * d4);
-  const int Sk = p.group_shared[k], chunk = prefix_chunk(Sk, p);
+  const int Sk = p.group_shared[k];
+  load_batch(0);
+  float S = M > -__builtin_inff() ? 1.f : 0.f;
+  const int chunk = prefix_chunk(Sk, p);
   const int chunks = (Sk + chunk - 1) / chunk;
-  const int64_t item0 = ((int64_t)k * p.num_kv_heads + g) * p.cmax;
-  constexpr int BATCH = 4;  // partials loaded per batch, all loads first
   for (int c0 = 0; c0 < chunks; c0 += BATCH) {
-    float2 ml[BATCH];
-    f32x4 o[BATCH];
+    if (c0 > 0) load_batch(c0);
 #pragma unroll
     for (int i = 0; i < BATCH; ++i) {
-      ml[i] = make_float2(-__builtin_inff(), 0.f);
-      o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (c0 + i < chunks) {
-        const int64_t slot = (item0 + c0 + i) * MG + m * G + h;
-        ml[i] = p.part_ml[slot];
-        o[i] = *(const f32x4*)(p.part_o + slot * D + 4 * d4);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < BATCH; ++i) {
+      if (c0 + i >= chunks) ml[i].x = -__builtin_inff();  // past the group's chunks
       if (ml[i].x > M) {
         const float sc = __builtin_amdgcn_exp2f(M - ml[i].x);
         acc = acc * sc + o[i];

@@ -116,8 +116,8 @@ def summarize_trace(d, workload, grpo=False):
         head = ["# rocprofv3 kernel trace: GRPO batch, plain and grouped decode", "",
                 "Command (repo root as $REPO):", "", "    " + GRPO_TRACE_CMD, "",
                 "`decode_kernel<..., false>` is the plain path; the grouped call runs",
-                "`prefix_kernel`, `decode_kernel<..., true>` (the suffix), the combine",
-                "kernel and `merge_kernel`.  Per-kernel durations from",
+                "`prefix_kernel`, `decode_kernel<..., true>` (the suffix) and",
+                "`combine_grouped_kernel`.  Per-kernel durations from",
                 "`run_kernel_stats.csv` (all dispatches: warm-up and timed calls).", ""]
     else:
         out = os.path.join(PROFILES, f"decode_kernel_{workload}_trace.md")

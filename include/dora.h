@@ -178,11 +178,11 @@ dora_status dora_decode_attn(const dora_decode_desc* desc,
  * leading pages that every member of group k holds in full (j < seq_len /
  * page_size) under the same page id as the group's first member; a group of
  * one shares nothing.  Any batch is valid input (S_k = 0 where nothing is
- * shared).  Steps, all enqueued on `stream`, no host round trip: a plan kernel
- * (S_k and each member's block-table row and length past it); a prefix kernel
- * (per group, KV head and chunk of shared pages: pages staged in LDS once,
- * applied to every member's query heads); the ordinary decode over each
- * member's remaining pages, in fp32 with log-sum-exp; a merge kernel. */
+ * shared).  Steps, all enqueued on `stream`, no host round trip: a prefix
+ * kernel (per group, KV head and chunk of shared pages: finds S_k, stages the
+ * pages in LDS once and applies them to every member's query heads); the
+ * ordinary decode over each member's remaining pages; its combine, which
+ * merges cut segments and folds every row with its group's prefix into out. */
 size_t dora_decode_grouped_workspace_bytes(const dora_decode_desc* desc, int32_t group_size);
 dora_status dora_decode_attn_grouped(const dora_decode_desc* desc, const void* q,
                                      const void* k_pages, const void* v_pages,

@@ -147,7 +147,7 @@ dora_status validate_tables(const dora_decode_desc& d, const int32_t* block_tabl
 // max(ceil(T / (K * Hkv)), ceil(stride / kPrefixMaxChunk))) chunks.
 struct GroupedLayout {
   WsLayout dec;
-  size_t gshared_off, part_o_off, part_ml_off, out32_off, lse_off, total;
+  size_t gshared_off, part_o_off, part_ml_off, out32_off, lse_off, seg_cut_off, total;
   int64_t cmax, items;
 };
 
@@ -176,6 +176,9 @@ bool grouped_layout(const dora_decode_desc& d, int32_t group_size, GroupedLayout
   off = align_up(off + (size_t)d.num_seqs * d.num_q_heads * d.head_dim * 4);
   L->lse_off = off;
   off = align_up(off + (size_t)d.num_seqs * d.num_q_heads * 4);
+  L->seg_cut_off = off;  // one launch's segments: reused by every launch
+  const int64_t seqs = d.num_seqs < kMaxSeqsPerLaunch ? d.num_seqs : kMaxSeqsPerLaunch;
+  off = align_up(off + (size_t)seqs * d.num_kv_heads * 4);
   L->total = off;
   return true;
 }
@@ -195,9 +198,9 @@ dora_status check_groups(const dora_decode_desc& d, int32_t group_size) {
 // skip[b / skip_group].
 dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void* k_pages,
                            const void* v_pages, const int32_t* block_table,
-                           const int32_t* seq_lens, uint16_t* out, float* out32, float* lse,
-                           const int32_t* skip, int32_t skip_group, uint8_t* ws,
-                           const WsLayout& w, hipStream_t s, hipEvent_t* ev) {
+                           const int32_t* seq_lens, uint16_t* out, const GroupedSuffix* gs,
+                           uint8_t* ws, const WsLayout& w, hipStream_t s, hipEvent_t* ev) {
+  const GroupedParams* gp = gs ? gs->gp : nullptr;
   const bool fp8 = d.kv_dtype == DORA_KV_FP8_E4M3;
   const int G = d.num_q_heads / d.num_kv_heads;
   const int e = fp8 ? 1 : 2;
@@ -214,12 +217,13 @@ dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void*
     dp.v_scales = d.v_scales;
     dp.block_table = block_table + (int64_t)c0 * d.block_table_stride;
     dp.seq_lens = seq_lens + c0;
-    dp.out = out ? out + c0 * qrow : nullptr;
-    dp.out32 = out32 ? out32 + c0 * qrow : nullptr;
-    dp.lse = lse ? lse + (int64_t)c0 * d.num_q_heads : nullptr;
-    dp.skip = skip;
+    dp.out = gp ? nullptr : out + c0 * qrow;
+    dp.out32 = gp ? gp->out32 + c0 * qrow : nullptr;
+    dp.lse = gp ? gp->lse + (int64_t)c0 * d.num_q_heads : nullptr;
+    dp.skip = gp ? gp->group_shared : nullptr;
     dp.skip_seq0 = c0;
-    dp.skip_group = skip_group;
+    dp.skip_group = gp ? gp->group_size : 1;
+    dp.seg_cut = gs ? gs->seg_cut : nullptr;
     dp.cuts = (int4*)(ws + w.cuts_off);
     dp.part_o = (float*)(ws + w.part_o_off);
     dp.part_ml = (float2*)(ws + w.part_ml_off);
@@ -234,9 +238,35 @@ dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void*
     if (launch_decode(dp, d.head_dim, d.page_size, fp8, w.waves, s) != hipSuccess)
       return DORA_ERR_HIP;
     if (ev && c0 == 0 && hipEventRecord(ev[1], s) != hipSuccess) return DORA_ERR_HIP;
-    CombineParams cp{dp.cuts, dp.part_o, dp.part_ml, dp.out, dp.out32, dp.lse, d.num_q_heads, G,
-                     d.head_dim};
-    if (launch_combine(cp, w.waves, s) != hipSuccess) return DORA_ERR_HIP;
+    CombineParams cp{};
+    cp.cuts = dp.cuts;
+    cp.part_o = dp.part_o;
+    cp.part_ml = dp.part_ml;
+    cp.num_q_heads = d.num_q_heads;
+    cp.group = G;
+    cp.head_dim = d.head_dim;
+    if (!gp) {
+      cp.out = dp.out;
+      if (launch_combine(cp, w.waves, s) != hipSuccess) return DORA_ERR_HIP;
+    } else {
+      cp.out = gp->out + c0 * qrow;
+      cp.out32 = dp.out32;
+      cp.lse = dp.lse;
+      cp.seg_cut = dp.seg_cut;
+      cp.group_shared = gp->group_shared;
+      cp.pre_o = gp->part_o;
+      cp.pre_ml = gp->part_ml;
+      cp.waves = (int32_t)w.waves;
+      cp.num_seqs = nb;
+      cp.seq0 = c0;
+      cp.num_kv_heads = d.num_kv_heads;
+      cp.group_size = gp->group_size;
+      cp.cmax = gp->cmax;
+      cp.pre_kh = (int64_t)(d.num_seqs / gp->group_size) * d.num_kv_heads;
+      const int64_t segs = (int64_t)nb * d.num_kv_heads;
+      if (launch_combine_grouped(cp, w.waves > segs ? w.waves : segs, s) != hipSuccess)
+        return DORA_ERR_HIP;
+    }
   }
   if (ev && hipEventRecord(ev[2], s) != hipSuccess) return DORA_ERR_HIP;
   return DORA_OK;
@@ -277,7 +307,7 @@ dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const 
   }
 
   return enqueue_decode(d, q, k_pages, v_pages, block_table, seq_lens, (uint16_t*)out, nullptr,
-                        nullptr, nullptr, 1, ws, w, s, ev);
+                        ws, w, s, ev);
 }
 
 size_t dora_decode_grouped_workspace_bytes(const dora_decode_desc* desc, int32_t group_size) {
@@ -347,10 +377,9 @@ dora_status dora_decode_attn_grouped(const dora_decode_desc* desc, const void* q
   gp.page_bytes = (int64_t)d.num_kv_heads * d.page_size * d.head_dim * e;
   gp.scale_log2 = scale * 1.4426950408889634f;
   if (launch_grouped_prefix(gp, (int)L.items, fp8, s) != hipSuccess) return DORA_ERR_HIP;
-  st = enqueue_decode(d, q, k_pages, v_pages, block_table, seq_lens, nullptr, gp.out32, gp.lse,
-                      gp.group_shared, group_size, ws, L.dec, s, nullptr);
-  if (st != DORA_OK) return st;
-  return launch_grouped_merge(gp, s) == hipSuccess ? DORA_OK : DORA_ERR_HIP;
+  const GroupedSuffix gs{&gp, (int32_t*)(ws + L.seg_cut_off)};
+  return enqueue_decode(d, q, k_pages, v_pages, block_table, seq_lens, nullptr, &gs, ws, L.dec, s,
+                        nullptr);
 }
 
 dora_status dora_kv_append(const dora_decode_desc* desc, const void* k_new, const void* v_new,

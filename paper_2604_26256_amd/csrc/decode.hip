@@ -35,7 +35,9 @@
 //            holds (at most one: its last segment), and writes the zero output
 //            of a share of the empty sequences.
 //   combine  one workgroup per wavefront: the log-sum-exp merge of the pieces
-//            of the cut segment that wavefront recorded.
+//            of the cut segment that wavefront recorded.  The grouped
+//            decode's variant also folds every row with the partials of its
+//            group's shared prefix.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -155,6 +157,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
       float* o = p.out32 + (int64_t)b * Hq * D;
       for (int e = lane; e < Hq * D; e += 64) o[e] = 0.f;
       for (int e = lane; e < Hq; e += 64) p.lse[(int64_t)b * Hq + e] = -__builtin_inff();
+      for (int e = lane; e < Hkv; e += 64) p.seg_cut[(int64_t)b * Hkv + e] = 0;
       continue;
     }
     uint32_t* o = (uint32_t*)(p.out + (int64_t)b * Hq * D);
@@ -269,6 +272,10 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
         if (grp == 0) p.part_ml[slot * G + col] = make_float2(m_run, l_tot);
       }
     }
+    if constexpr (SUFFIX) {  // which rows the combine takes from out32 / lse
+      if (lane == 0 && (seg_whole || seg_here))
+        p.seg_cut[(int64_t)seg_b * Hkv + seg_g] = seg_whole ? 0 : 1;
+    }
     if (!seg_whole && seg_here) {
       // pieces of this segment: ranges w .. the range of its last page-head
       const int nb = sN[seg_b + 1] - sN[seg_b];
@@ -365,6 +372,52 @@ done:
 constexpr int kCombineThreads = 1024;
 constexpr int kCombineBatch = 4;  // pieces whose loads a thread issues together
 
+// Online log-sum-exp merge of one piece (max in log2 units, sum, unnormalised
+// weighted values) into a running (M, S, acc).
+__device__ __forceinline__ void merge_piece(float2 ml, f32x4 o, float& M, float& S, f32x4& acc) {
+  if (ml.x > M) {
+    const float sc = __builtin_amdgcn_exp2f(M - ml.x);
+    acc = acc * sc + o;
+    S = S * sc + ml.y;
+    M = ml.x;
+  } else if (ml.x > -__builtin_inff()) {
+    const float w = __builtin_amdgcn_exp2f(ml.x - M);
+    acc += w * o;
+    S += w * ml.y;
+  }
+}
+
+// Grouped decode: thread group sg of `groups` folds chunks c = sg, sg +
+// groups, ... of the prefix partials of (member, head n) of segment (b, g)
+// into its running (M, S, acc); Sk is the group's shared page count.
+__device__ __forceinline__ void fold_prefix_chunks(const CombineParams& p, int b, int g, int n,
+                                                   int d4, int Sk, int sg, int groups, float& M,
+                                                   float& S, f32x4& acc) {
+  const int G = p.group, D = p.head_dim, Mg = p.group_size, MG = Mg * G;
+  const int64_t bb = (int64_t)p.seq0 + b;  // index in the whole batch
+  const int k = (int)(bb / Mg), m = (int)(bb - (int64_t)k * Mg);
+  const int64_t item0 = ((int64_t)k * p.num_kv_heads + g) * p.cmax;
+  const int chunk = prefix_chunk_of(Sk, p.pre_kh);
+  const int chunks = (Sk + chunk - 1) / chunk;
+  for (int c0 = sg; c0 < chunks; c0 += groups * kCombineBatch) {
+    float2 ml[kCombineBatch];
+    f32x4 o[kCombineBatch];
+#pragma unroll
+    for (int i = 0; i < kCombineBatch; ++i) {  // all loads of the batch first
+      const int c = c0 + i * groups;
+      ml[i] = make_float2(-__builtin_inff(), 0.f);
+      o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (c < chunks) {
+        const int64_t slot = (item0 + c) * MG + m * G + n;
+        ml[i] = p.pre_ml[slot];
+        o[i] = *(const f32x4*)(p.pre_o + slot * D + 4 * d4);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kCombineBatch; ++i) merge_piece(ml[i], o[i], M, S, acc);
+  }
+}
+
 // One workgroup per decode wavefront w.  If w recorded a cut segment, its np
 // pieces sit in the slots of wavefronts w .. w+np-1: w's in 2w + first_off,
 // every later one's in 2w'.  Threads are (head, 4 head-dim values) tasks x
@@ -446,6 +499,110 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(CombineParams 
   }
 }
 
+// The combine of the grouped decode's suffix: as combine_kernel, with the
+// chunk partials of the group's shared prefix folded in as further pieces;
+// and workgroup i < B * Hkv also writes the rows of segment (b, g) =
+// (i / Hkv, i % Hkv) if the decode finished that segment whole (out32 / lse),
+// folded with its prefix the same way.  The launch has max(wavefronts,
+// B * Hkv) workgroups.
+__global__ __launch_bounds__(kCombineThreads) void combine_grouped_kernel(CombineParams p) {
+  __shared__ float sM[kCombineThreads], sS[kCombineThreads];
+  __shared__ f32x4 sAcc[kCombineThreads];
+  const int t = threadIdx.x;
+  const int G = p.group, D = p.head_dim;
+  const int tasks = G * (D / 4);
+  const int tasks_r = (tasks + 63) & ~63;
+  const int groups = kCombineThreads / tasks_r;  // >= 2 since tasks <= 512
+  const int task = t % tasks_r, sg = t / tasks_r;
+  const bool active = task < tasks && sg < groups;
+  const int n = active ? task / (D / 4) : 0, d4 = active ? task - n * (D / 4) : 0;
+  // merges the groups' (M, S, acc) in LDS; returns the row in thread group 0
+  auto merge_groups = [&](float M, float S, f32x4 acc, float& Mx, float& den, f32x4& num) {
+    sM[t] = M;
+    sS[t] = S;
+    sAcc[t] = acc;
+    __syncthreads();
+    if (sg == 0 && task < tasks) {
+      Mx = M;
+      for (int k = 1; k < groups; ++k) Mx = fmaxf(Mx, sM[k * tasks_r + task]);
+      num = f32x4{0.f, 0.f, 0.f, 0.f};
+      den = 0.f;
+      for (int k = 0; k < groups; ++k) {
+        const int i = k * tasks_r + task;
+        if (sM[i] == -__builtin_inff()) continue;  // a group with no pieces
+        const float sc = __builtin_amdgcn_exp2f(sM[i] - Mx);
+        num += sc * sAcc[i];
+        den += sc * sS[i];
+      }
+    }
+  };
+  auto store_row = [&](int b, int g, f32x4 num, float den) {
+    const float inv = den > 0.f ? 1.f / den : 0.f;
+    const int64_t row = (int64_t)b * p.num_q_heads + g * G + n;
+    *(bf16x4*)(p.out + row * D + 4 * d4) =
+        bf16x4{(__bf16)(num[0] * inv), (__bf16)(num[1] * inv), (__bf16)(num[2] * inv),
+               (__bf16)(num[3] * inv)};
+  };
+  if ((int)blockIdx.x < p.waves) {
+    const int4 cut = p.cuts[blockIdx.x];
+    if (cut.x >= 0) {  // uniform
+      const int64_t wa = blockIdx.x;
+      const int b = cut.x, g = cut.y, np = cut.z, first_off = cut.w;
+      const int Sk = p.group_shared[(p.seq0 + b) / p.group_size];
+      float M = -__builtin_inff(), S = 0.f;
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (active) {
+        for (int k0 = sg; k0 < np; k0 += groups * kCombineBatch) {
+          float2 ml[kCombineBatch];
+          f32x4 o[kCombineBatch];
+#pragma unroll
+          for (int i = 0; i < kCombineBatch; ++i) {  // all loads of the batch first
+            const int k = k0 + i * groups;
+            ml[i] = make_float2(-__builtin_inff(), 0.f);
+            o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (k < np) {
+              const int64_t row = (2 * (wa + k) + (k == 0 ? first_off : 0)) * G + n;
+              ml[i] = p.part_ml[row];
+              o[i] = *(const f32x4*)(p.part_o + row * D + 4 * d4);
+            }
+          }
+#pragma unroll
+          for (int i = 0; i < kCombineBatch; ++i) merge_piece(ml[i], o[i], M, S, acc);
+        }
+        fold_prefix_chunks(p, b, g, n, d4, Sk, sg, groups, M, S, acc);
+      }
+      float Mx, den;
+      f32x4 num;
+      merge_groups(M, S, acc, Mx, den, num);
+      if (sg == 0 && task < tasks) store_row(b, g, num, den);
+    }
+  }
+  // Segment (b, g) finished whole by the decode: its normalised rows in
+  // out32 with weight 2^lse, as the first piece of thread group 0.
+  if ((int64_t)blockIdx.x < (int64_t)p.num_seqs * p.num_kv_heads) {  // uniform
+    const int b = (int)blockIdx.x / p.num_kv_heads, g = (int)blockIdx.x - b * p.num_kv_heads;
+    if (p.seg_cut[blockIdx.x] == 0) {  // uniform
+      __syncthreads();  // LDS reuse after a cut record's merge
+      const int Sk = p.group_shared[(p.seq0 + b) / p.group_size];
+      float M = -__builtin_inff(), S = 0.f;
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (active) {
+        if (sg == 0) {
+          const int64_t row = (int64_t)b * p.num_q_heads + g * G + n;
+          M = p.lse[row];
+          S = M > -__builtin_inff() ? 1.f : 0.f;
+          acc = *(const f32x4*)(p.out32 + row * D + 4 * d4);
+        }
+        fold_prefix_chunks(p, b, g, n, d4, Sk, sg, groups, M, S, acc);
+      }
+      float Mx, den;
+      f32x4 num;
+      merge_groups(M, S, acc, Mx, den, num);
+      if (sg == 0 && task < tasks) store_row(b, g, num, den);
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // validate (DORA_FLAG_VALIDATE): page ids in range and owned by the version
 // ---------------------------------------------------------------------------
@@ -522,6 +679,13 @@ hipError_t launch_decode(const DecodeParams& p, int head_dim, int page_size, boo
 hipError_t launch_combine(const CombineParams& p, int64_t waves, hipStream_t s) {
   if (waves <= 0) return hipSuccess;
   hipLaunchKernelGGL(combine_kernel, dim3((unsigned)waves), dim3(kCombineThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_grouped(const CombineParams& p, int64_t grid, hipStream_t s) {
+  if (grid <= 0) return hipSuccess;
+  hipLaunchKernelGGL(combine_grouped_kernel, dim3((unsigned)grid), dim3(kCombineThreads), 0, s,
+                     p);
   return hipGetLastError();
 }
 

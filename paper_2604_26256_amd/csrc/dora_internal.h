@@ -57,6 +57,7 @@ struct DecodeParams {
   int32_t min_range;   // smallest range in page-heads
   int64_t page_bytes;  // bytes of one K (or V) page, all KV heads
   float scale_log2;    // softmax scale times log2(e)
+  int32_t* seg_cut;    // with out32: [B][Hkv] 1 where the segment was cut, else 0
 };
 
 struct CombineParams {
@@ -64,9 +65,19 @@ struct CombineParams {
   const float* part_o;
   const float2* part_ml;
   uint16_t* out;
-  float* out32;  // as in DecodeParams
+  float* out32;  // if set (and not grouped): fp32 rows and their log-sum-exp
   float* lse;
   int32_t num_q_heads, group, head_dim;
+  // Grouped decode only: every row of this launch's sequences is folded with
+  // its group's prefix partials before the bf16 store.  Rows the decode
+  // finished whole come from out32 / lse; cut ones from the pieces.
+  const int32_t* seg_cut;       // [num_seqs][num_kv_heads], from the decode
+  const int32_t* group_shared;  // per group: shared full pages
+  const float* pre_o;           // prefix partials, as GroupedParams::part_o
+  const float2* pre_ml;
+  int32_t waves;                // decode wavefronts (cut records)
+  int32_t num_seqs, seq0, num_kv_heads, group_size, cmax;
+  int64_t pre_kh;               // groups x KV heads of the whole batch
 };
 
 // Grouped decode (groups of sequences sharing a prompt's pages).
@@ -74,6 +85,18 @@ constexpr int kPrefixMaxWaves = 8;      // (member, head) columns per group <= 1
 constexpr int kPrefixMinChunk = 16;     // shared pages per prefix work item, at least ...
 constexpr int kPrefixMaxChunk = 512;    // ... and at most
 constexpr int kPrefixTargetItems = 512; // prefix work items aimed at (2 per CU)
+
+// Pages per prefix work item of a group sharing S pages, with kh (group, KV
+// head) pairs in the batch: about kPrefixTargetItems items over all pairs,
+// clamped to [kPrefixMinChunk, kPrefixMaxChunk].  Item (k, g, c) covers pages
+// [c * chunk, min((c + 1) * chunk, S)); its partials sit at item index
+// (k * Hkv + g) * cmax + c.  The prefix kernel and the folding combine both
+// derive the split from here.
+__host__ __device__ inline int prefix_chunk_of(int S, int64_t kh) {
+  const int64_t want = ((int64_t)S * kh + kPrefixTargetItems - 1) / kPrefixTargetItems;
+  return want < kPrefixMinChunk ? kPrefixMinChunk
+                                : (want > kPrefixMaxChunk ? kPrefixMaxChunk : (int)want);
+}
 
 struct GroupedParams {
   const uint16_t* q;
@@ -97,12 +120,17 @@ struct GroupedParams {
 };
 
 hipError_t launch_grouped_prefix(const GroupedParams& p, int grid, bool fp8, hipStream_t s);
-hipError_t launch_grouped_merge(const GroupedParams& p, hipStream_t s);
+// The suffix decode of the grouped path: out32 / lse hold rows the decode
+// finishes whole, seg_cut which segments were cut; the combine then writes
+// every row to gp.out folded with the prefix partials.
+struct GroupedSuffix {
+  const GroupedParams* gp;
+  int32_t* seg_cut;  // [min(B, kMaxSeqsPerLaunch)][Hkv], reused per launch
+};
 dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void* k_pages,
                            const void* v_pages, const int32_t* block_table,
-                           const int32_t* seq_lens, uint16_t* out, float* out32, float* lse,
-                           const int32_t* skip, int32_t skip_group, uint8_t* ws,
-                           const WsLayout& w, hipStream_t s, hipEvent_t* ev);
+                           const int32_t* seq_lens, uint16_t* out, const GroupedSuffix* gs,
+                           uint8_t* ws, const WsLayout& w, hipStream_t s, hipEvent_t* ev);
 
 struct ValidateParams {
   const int32_t* block_table;
@@ -119,6 +147,7 @@ hipError_t decode_waves_per_cu(int head_dim, int page_size, bool fp8, int num_se
 hipError_t launch_decode(const DecodeParams& p, int head_dim, int page_size, bool fp8,
                          int64_t waves, hipStream_t s);
 hipError_t launch_combine(const CombineParams& p, int64_t waves, hipStream_t s);
+hipError_t launch_combine_grouped(const CombineParams& p, int64_t grid, hipStream_t s);
 hipError_t launch_validate(const ValidateParams& p, hipStream_t s);
 
 struct AppendParams {

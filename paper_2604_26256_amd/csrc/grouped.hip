@@ -14,9 +14,9 @@
 //            kernel's MFMA/online-softmax step, and writes an unnormalised
 //            partial (o, running max, sum) per column.
 //   suffix   the decode kernel over each member's pages past S, writing fp32
-//            rows and their log-sum-exp.
-//   merge    per (sequence, KV head): the chunk partials of its prefix and its
-//            suffix row folded into the bf16 output.
+//            rows and their log-sum-exp for the segments it finishes whole;
+//            its combine merges the cut ones and folds every row with the
+//            chunk partials of its group's prefix into the bf16 output.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -64,17 +64,9 @@ __device__ int shared_prefix(const GroupedParams& p, int k, int enough) {
   return s_min < cap ? s_min : cap;
 }
 
-// Pages per prefix work item of a group sharing S pages: about
-// kPrefixTargetItems items over all K * Hkv (group, KV head) pairs, clamped to
-// [kPrefixMinChunk, kPrefixMaxChunk].  Item (k, g, c) covers pages
-// [c * chunk, min((c + 1) * chunk, S)); its partials sit at item index
-// (k * Hkv + g) * cmax + c.  The prefix and merge kernels both derive the
-// split from here.
+// The split of a group's shared pages into work items: prefix_chunk_of.
 __device__ __forceinline__ int prefix_chunk(int S, const GroupedParams& p) {
-  const int64_t kh = (int64_t)(p.num_seqs / p.group_size) * p.num_kv_heads;
-  const int64_t want = ((int64_t)S * kh + kPrefixTargetItems - 1) / kPrefixTargetItems;
-  return want < kPrefixMinChunk ? kPrefixMinChunk
-                                : (want > kPrefixMaxChunk ? kPrefixMaxChunk : (int)want);
+  return prefix_chunk_of(S, (int64_t)(p.num_seqs / p.group_size) * p.num_kv_heads);
 }
 
 // One step consumes PAIR consecutive pages as one virtual page of VP = PAIR * P
@@ -124,7 +116,7 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(GroupedParams p)
   }
 
   // The group's shared prefix; the first workgroup of each group publishes it
-  // for the suffix decode and the merge.  A chunk that starts past every
+  // for the suffix decode and its combine.  A chunk that starts past every
   // member's full pages has no work whatever the prefix is.
   const int S = shared_prefix(p, k, c * kPrefixMinChunk);
   if (c == 0 && g == 0 && threadIdx.x == 0) {
@@ -254,61 +246,6 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(GroupedParams p)
   }
 }
 
-// Merge, one workgroup per (sequence, KV head); thread = (head, 4 dims).  The
-// suffix row, the group's prefix length and the first BATCH chunk partials are
-// loaded together: slots past the group's chunk count lie inside the
-// (group, KV head)'s cmax slots and are read and dropped, so the common case
-// (at most BATCH chunks) costs one round trip.
-__global__ __launch_bounds__(512) void merge_kernel(GroupedParams p) {
-  const int b = blockIdx.x / p.num_kv_heads, g = blockIdx.x - b * p.num_kv_heads;
-  const int G = p.group, D = p.head_dim, MG = p.group_size * G;
-  const int h = threadIdx.x / (D / 4), d4 = threadIdx.x - h * (D / 4);
-  if (h >= G) return;
-  const int k = b / p.group_size, m = b - k * p.group_size;
-  const int64_t row = (int64_t)b * p.num_q_heads + (int64_t)g * G + h;
-  const int64_t item0 = ((int64_t)k * p.num_kv_heads + g) * p.cmax;
-  constexpr int BATCH = 16;
-  float2 ml[BATCH];
-  f32x4 o[BATCH];
-  auto load_batch = [&](int c0) {
-#pragma unroll
-    for (int i = 0; i < BATCH; ++i) {
-      const int c = c0 + i < p.cmax ? c0 + i : p.cmax - 1;
-      const int64_t slot = (item0 + c) * MG + m * G + h;
-      ml[i] = p.part_ml[slot];
-      o[i] = *(const f32x4*)(p.part_o + slot * D + 4 * d4);
-    }
-  };
-  // the suffix row (normalised) as a piece of weight 2^lse
-  float M = p.lse[row];
-  f32x4 acc = *(const f32x4*)(p.out32 + row * D + 4 * d4);
-  const int Sk = p.group_shared[k];
-  load_batch(0);
-  float S = M > -__builtin_inff() ? 1.f : 0.f;
-  const int chunk = prefix_chunk(Sk, p);
-  const int chunks = (Sk + chunk - 1) / chunk;
-  for (int c0 = 0; c0 < chunks; c0 += BATCH) {
-    if (c0 > 0) load_batch(c0);
-#pragma unroll
-    for (int i = 0; i < BATCH; ++i) {
-      if (c0 + i >= chunks) ml[i].x = -__builtin_inff();  // past the group's chunks
-      if (ml[i].x > M) {
-        const float sc = __builtin_amdgcn_exp2f(M - ml[i].x);
-        acc = acc * sc + o[i];
-        S = S * sc + ml[i].y;
-        M = ml[i].x;
-      } else if (ml[i].x > -__builtin_inff()) {
-        const float w = __builtin_amdgcn_exp2f(ml[i].x - M);
-        acc += w * o[i];
-        S += w * ml[i].y;
-      }
-    }
-  }
-  const float inv = S > 0.f ? 1.f / S : 0.f;
-  *(bf16x4*)(p.out + row * D + 4 * d4) = bf16x4{(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv),
-                                              (__bf16)(acc[2] * inv), (__bf16)(acc[3] * inv)};
-}
-
 template <int D, int P, bool FP8>
 static const void* prefix_fn() {
   return (const void*)&prefix_kernel<D, P, FP8>;
@@ -326,12 +263,6 @@ hipError_t launch_grouped_prefix(const GroupedParams& p, int grid, bool fp8, hip
   GroupedParams arg = p;
   void* args[] = {(void*)&arg};
   return hipLaunchKernel(fn, dim3((unsigned)grid), dim3(kPrefixThreads), args, 0, s);
-}
-
-hipError_t launch_grouped_merge(const GroupedParams& p, hipStream_t s) {
-  hipLaunchKernelGGL(merge_kernel, dim3(p.num_seqs * p.num_kv_heads),
-                     dim3(p.group * (p.head_dim / 4)), 0, s, p);
-  return hipGetLastError();
 }
 
 }  // namespace dora

@@ -471,9 +471,10 @@ def copy_bandwidth(torch, nbytes=2 << 30):
     return out
 
 
-def cpu_baseline(b, budget_s=20.0):
+def cpu_baseline(b, budget_s=20.0, min_s=10.0):
     """The fp64 oracle on the host cores over the same batch (or a prefix of
-    its sequences that fits the time budget), scaled to decode tokens/s."""
+    its sequences that fits the time budget), repeated until min_s of work is
+    timed, scaled to decode tokens/s."""
     import oracle
 
     cores = min(16, len(os.sched_getaffinity(0)))
@@ -493,19 +494,25 @@ def cpu_baseline(b, budget_s=20.0):
         if acc >= budget_s:
             break
     sub = wl.subset_for_oracle(b, take)
-    t0 = time.perf_counter()
-    oracle.decode(sub["q"], sub["k_pages"], sub["v_pages"], sub["block_table"],
-                  sub["seq_lens"], num_kv_heads=b.w.num_kv_heads, page_size=b.w.page_size,
-                  kv_dtype=b.w.kv_dtype, k_scales=sub["k_scales"], v_scales=sub["v_scales"],
-                  num_pages=sub["num_pages"], nthreads=cores)
-    dt = time.perf_counter() - t0
+    # repeat the sample until at least min_s of CPU time is measured
+    reps, total = 0, 0.0
+    while reps == 0 or total < min_s:
+        t0 = time.perf_counter()
+        oracle.decode(sub["q"], sub["k_pages"], sub["v_pages"], sub["block_table"],
+                      sub["seq_lens"], num_kv_heads=b.w.num_kv_heads, page_size=b.w.page_size,
+                      kv_dtype=b.w.kv_dtype, k_scales=sub["k_scales"], v_scales=sub["v_scales"],
+                      num_pages=sub["num_pages"], nthreads=cores)
+        total += time.perf_counter() - t0
+        reps += 1
+    dt = total / reps
     ctx = int(b.lengths[take].sum())
     # one decode step of the whole batch costs sum(L) context tokens of work
     step_s = dt * float(b.lengths.sum()) / ctx
     return {"value": b.w.num_seqs / step_s, "unit": "tokens/s", "cores": cores,
             "kind": "oracle",
-            "sample": f"{len(take)} of {b.w.num_seqs} sequences ({ctx} context tokens, "
-                      f"{dt:.2f} s), scaled by total/sampled context tokens",
+            "sample": f"{len(take)} of {b.w.num_seqs} sequences ({ctx} context tokens), "
+                      f"run {reps} times ({total:.1f} s, {dt:.3f} s each), scaled by "
+                      f"total/sampled context tokens",
             "cpu_model": _cpu_model()}
 
 

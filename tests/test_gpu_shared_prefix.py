@@ -94,6 +94,32 @@ def test_grouped_is_deterministic():
         assert torch.equal(_grouped(b, 4)[0], a)
 
 
+@pytest.mark.parametrize("fill", [0x00, 0xFF, 0x7F])
+def test_grouped_workspace_contents_ignored(fill):
+    """Every per-call value the grouped kernels read back (the prefix lengths,
+    partials, suffix rows and the whole-or-cut flag of each segment) is written
+    earlier in the same call: a workspace filled with zeros (every segment
+    'whole'), all-ones bytes (every flag set, NaN partials) or 0x7F bytes
+    gives the bit-identical output of a fresh workspace, with segments both
+    whole and cut (a range of 8 page-heads cuts most of them)."""
+    print(f"[case] grouped workspace fill {fill:#x}", flush=True)
+    w = wl.Workload("ws", 12, 28, 4, 128, 16, 0, 8192, "lognormal", 300, 1.0, 1, 2500)
+    b, shared = wl.make_grpo_batch(w, group_size=4, prompt_range=(100, 900), device="cuda",
+                                   seed_index=45)
+    d = lib()
+    desc = d.make_decode_desc(num_seqs=w.num_seqs, num_q_heads=w.num_q_heads,
+                              num_kv_heads=w.num_kv_heads, head_dim=w.head_dim,
+                              page_size=w.page_size, block_table_stride=b.block_table.shape[1],
+                              num_pages=w.num_pages, kv_dtype=0)
+    need = d.dora_decode_grouped_workspace_bytes(desc, 4)
+    ref, _ = _grouped(b, 4, workspace=torch.zeros(need, dtype=torch.uint8, device="cuda"))
+    ws = torch.full((need,), fill, dtype=torch.uint8, device="cuda")
+    out, det = _grouped(b, 4, workspace=ws)
+    assert det.tolist() == shared[::4].tolist()
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+    assert max_abs_err(out, oracle_for(b)) <= TOL[0]
+
+
 def test_grouped_full_size_grpo_batch_sampled():
     b, shared = wl.make_grpo_batch(device="cuda")
     out, det = _grouped(b, wl.GRPO_GROUP)

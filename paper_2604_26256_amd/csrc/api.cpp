@@ -147,7 +147,7 @@ dora_status validate_tables(const dora_decode_desc& d, const int32_t* block_tabl
 // max(ceil(T / (K * Hkv)), ceil(stride / kPrefixMaxChunk))) chunks.
 struct GroupedLayout {
   WsLayout dec;
-  size_t gshared_off, part_o_off, part_ml_off, out32_off, lse_off, seg_cut_off, total;
+  size_t gshared_off, part_o_off, part_ml_off, out32_off, lse_off, seg_rec_off, total;
   int64_t cmax, items;
 };
 
@@ -176,9 +176,9 @@ bool grouped_layout(const dora_decode_desc& d, int32_t group_size, GroupedLayout
   off = align_up(off + (size_t)d.num_seqs * d.num_q_heads * d.head_dim * 4);
   L->lse_off = off;
   off = align_up(off + (size_t)d.num_seqs * d.num_q_heads * 4);
-  L->seg_cut_off = off;  // one launch's segments: reused by every launch
+  L->seg_rec_off = off;  // one launch's segment records: reused by every launch
   const int64_t seqs = d.num_seqs < kMaxSeqsPerLaunch ? d.num_seqs : kMaxSeqsPerLaunch;
-  off = align_up(off + (size_t)seqs * d.num_kv_heads * 4);
+  off = align_up(off + (size_t)seqs * d.num_kv_heads * 16);
   L->total = off;
   return true;
 }
@@ -223,8 +223,11 @@ dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void*
     dp.skip = gp ? gp->group_shared : nullptr;
     dp.skip_seq0 = c0;
     dp.skip_group = gp ? gp->group_size : 1;
-    dp.seg_cut = gs ? gs->seg_cut : nullptr;
-    dp.cuts = (int4*)(ws + w.cuts_off);
+    // Cut records per segment where that is the smaller combine launch (the
+    // grouped combine always works per segment); per wavefront otherwise.
+    const int64_t segs = (int64_t)nb * d.num_kv_heads;
+    dp.seg_records = (gp || segs <= w.waves) ? 1 : 0;
+    dp.cuts = gs ? gs->seg_rec : (int4*)(ws + w.cuts_off);
     dp.part_o = (float*)(ws + w.part_o_off);
     dp.part_ml = (float2*)(ws + w.part_ml_off);
     dp.num_seqs = nb;
@@ -240,6 +243,7 @@ dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void*
     if (ev && c0 == 0 && hipEventRecord(ev[1], s) != hipSuccess) return DORA_ERR_HIP;
     CombineParams cp{};
     cp.cuts = dp.cuts;
+    cp.seg_records = dp.seg_records;
     cp.part_o = dp.part_o;
     cp.part_ml = dp.part_ml;
     cp.num_q_heads = d.num_q_heads;
@@ -247,24 +251,22 @@ dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void*
     cp.head_dim = d.head_dim;
     if (!gp) {
       cp.out = dp.out;
-      if (launch_combine(cp, w.waves, s) != hipSuccess) return DORA_ERR_HIP;
+      if (launch_combine(cp, dp.seg_records ? segs : w.waves, s) != hipSuccess)
+        return DORA_ERR_HIP;
     } else {
       cp.out = gp->out + c0 * qrow;
       cp.out32 = dp.out32;
       cp.lse = dp.lse;
-      cp.seg_cut = dp.seg_cut;
       cp.group_shared = gp->group_shared;
       cp.pre_o = gp->part_o;
       cp.pre_ml = gp->part_ml;
-      cp.waves = (int32_t)w.waves;
       cp.num_seqs = nb;
       cp.seq0 = c0;
       cp.num_kv_heads = d.num_kv_heads;
       cp.group_size = gp->group_size;
       cp.cmax = gp->cmax;
       cp.pre_kh = (int64_t)(d.num_seqs / gp->group_size) * d.num_kv_heads;
-      const int64_t segs = (int64_t)nb * d.num_kv_heads;
-      if (launch_combine_grouped(cp, w.waves > segs ? w.waves : segs, s) != hipSuccess)
+      if (launch_combine_grouped(cp, segs, s) != hipSuccess)
         return DORA_ERR_HIP;
     }
   }
@@ -377,7 +379,7 @@ dora_status dora_decode_attn_grouped(const dora_decode_desc* desc, const void* q
   gp.page_bytes = (int64_t)d.num_kv_heads * d.page_size * d.head_dim * e;
   gp.scale_log2 = scale * 1.4426950408889634f;
   if (launch_grouped_prefix(gp, (int)L.items, fp8, s) != hipSuccess) return DORA_ERR_HIP;
-  const GroupedSuffix gs{&gp, (int32_t*)(ws + L.seg_cut_off)};
+  const GroupedSuffix gs{&gp, (int4*)(ws + L.seg_rec_off)};
   return enqueue_decode(d, q, k_pages, v_pages, block_table, seq_lens, nullptr, &gs, ws, L.dec, s,
                         nullptr);
 }

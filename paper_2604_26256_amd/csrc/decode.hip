@@ -157,18 +157,20 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
       float* o = p.out32 + (int64_t)b * Hq * D;
       for (int e = lane; e < Hq * D; e += 64) o[e] = 0.f;
       for (int e = lane; e < Hq; e += 64) p.lse[(int64_t)b * Hq + e] = -__builtin_inff();
-      for (int e = lane; e < Hkv; e += 64) p.seg_cut[(int64_t)b * Hkv + e] = 0;
+      for (int e = lane; e < Hkv; e += 64) p.cuts[(int64_t)b * Hkv + e] = make_int4(-1, 0, 0, 0);
       continue;
     }
     uint32_t* o = (uint32_t*)(p.out + (int64_t)b * Hq * D);
     for (int e = lane; e < Hq * D / 2; e += 64) o[e] = 0u;
+    if (p.seg_records)
+      for (int e = lane; e < Hkv; e += 64) p.cuts[(int64_t)b * Hkv + e] = make_int4(-1, 0, 0, 0);
   }
 
   // 2. this wavefront's range of page-heads
   const int T = uni(Hkv * carry);  // fits in 32 bits: the host bounds batch x stride x Hkv
   const int W = uni(effective_waves(T, (int)gridDim.x, p.min_range));
   if (T == 0 || w >= W) {
-    if (lane == 0) p.cuts[w] = make_int4(-1, 0, 0, 0);
+    if (lane == 0 && !p.seg_records) p.cuts[w] = make_int4(-1, 0, 0, 0);
     return;
   }
   Split split;
@@ -272,10 +274,6 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
         if (grp == 0) p.part_ml[slot * G + col] = make_float2(m_run, l_tot);
       }
     }
-    if constexpr (SUFFIX) {  // which rows the combine takes from out32 / lse
-      if (lane == 0 && (seg_whole || seg_here))
-        p.seg_cut[(int64_t)seg_b * Hkv + seg_g] = seg_whole ? 0 : 1;
-    }
     if (!seg_whole && seg_here) {
       // pieces of this segment: ranges w .. the range of its last page-head
       const int nb = sN[seg_b + 1] - sN[seg_b];
@@ -283,6 +281,9 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
       const int np = split.range_of(s0 + nb - 1) - (int)w + 1;
       cut = make_int4(seg_b, seg_g, np, first_seg ? 0 : 1);
     }
+    if (p.seg_records && lane == 0 && (seg_whole || seg_here))  // the segment's record
+      p.cuts[(int64_t)seg_b * Hkv + seg_g] =
+          seg_whole ? make_int4(-1, 0, 0, 0) : make_int4((int)w, cut.z, cut.w, 0);
     first_seg = false;
   };
 
@@ -362,7 +363,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
     }
   }
 done:
-  if (lane == 0) p.cuts[w] = cut;
+  if (lane == 0 && !p.seg_records) p.cuts[w] = cut;
 }
 
 // ---------------------------------------------------------------------------
@@ -418,18 +419,29 @@ __device__ __forceinline__ void fold_prefix_chunks(const CombineParams& p, int b
   }
 }
 
-// One workgroup per decode wavefront w.  If w recorded a cut segment, its np
-// pieces sit in the slots of wavefronts w .. w+np-1: w's in 2w + first_off,
-// every later one's in 2w'.  Threads are (head, 4 head-dim values) tasks x
-// piece groups; each folds its pieces into a running (max, normaliser,
-// weighted sum) with one pass of loads, and the groups are merged in LDS.
+// One workgroup per cut record: per decode wavefront w, or per segment when
+// the records are kept per segment (batches with no more segments than
+// wavefronts, so the launch is smaller).  A cut segment's np pieces sit in
+// the slots of wavefronts wa .. wa+np-1, wa the wavefront holding its first
+// piece: wa's in 2wa + first_off, every later one's in 2w'.  Threads are
+// (head, 4 head-dim values) tasks x piece groups; each folds its pieces into
+// a running (max, normaliser, weighted sum) with one pass of loads, and the
+// groups are merged in LDS.
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(CombineParams p) {
   __shared__ float sM[kCombineThreads], sS[kCombineThreads];
   __shared__ f32x4 sAcc[kCombineThreads];
   const int4 cut = p.cuts[blockIdx.x];
   if (cut.x < 0) return;
-  const int64_t wa = blockIdx.x;
-  const int b = cut.x, g = cut.y, np = cut.z, first_off = cut.w;
+  int64_t wa = blockIdx.x;
+  int b = cut.x, g = cut.y, np = cut.z, first_off = cut.w;
+  if (p.seg_records) {  // workgroup per segment (b, g); the record names its first wavefront
+    const int Hkv = p.num_q_heads / p.group;
+    wa = cut.x;
+    np = cut.y;
+    first_off = cut.z;
+    b = (int)blockIdx.x / Hkv;
+    g = (int)blockIdx.x - b * Hkv;
+  }
   const int t = threadIdx.x;
   const int G = p.group, D = p.head_dim;
   const int tasks = G * (D / 4);
@@ -499,12 +511,13 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(CombineParams 
   }
 }
 
-// The combine of the grouped decode's suffix: as combine_kernel, with the
-// chunk partials of the group's shared prefix folded in as further pieces;
-// and workgroup i < B * Hkv also writes the rows of segment (b, g) =
-// (i / Hkv, i % Hkv) if the decode finished that segment whole (out32 / lse),
-// folded with its prefix the same way.  The launch has max(wavefronts,
-// B * Hkv) workgroups.
+// The combine of the grouped decode's suffix: one workgroup per segment (b, g)
+// of the launch, with the segment's cut record.  A cut segment's pieces are
+// merged as in combine_kernel; a segment the decode finished whole (or an
+// empty one) starts from its normalised rows in out32 with weight 2^lse
+// (loaded with the record, and dropped if the segment was cut).  Either way
+// the chunk partials of the group's shared prefix are folded in as further
+// pieces before the bf16 store.
 __global__ __launch_bounds__(kCombineThreads) void combine_grouped_kernel(CombineParams p) {
   __shared__ float sM[kCombineThreads], sS[kCombineThreads];
   __shared__ f32x4 sAcc[kCombineThreads];
@@ -516,90 +529,66 @@ __global__ __launch_bounds__(kCombineThreads) void combine_grouped_kernel(Combin
   const int task = t % tasks_r, sg = t / tasks_r;
   const bool active = task < tasks && sg < groups;
   const int n = active ? task / (D / 4) : 0, d4 = active ? task - n * (D / 4) : 0;
-  // merges the groups' (M, S, acc) in LDS; returns the row in thread group 0
-  auto merge_groups = [&](float M, float S, f32x4 acc, float& Mx, float& den, f32x4& num) {
-    sM[t] = M;
-    sS[t] = S;
-    sAcc[t] = acc;
-    __syncthreads();
-    if (sg == 0 && task < tasks) {
-      Mx = M;
-      for (int k = 1; k < groups; ++k) Mx = fmaxf(Mx, sM[k * tasks_r + task]);
-      num = f32x4{0.f, 0.f, 0.f, 0.f};
-      den = 0.f;
-      for (int k = 0; k < groups; ++k) {
-        const int i = k * tasks_r + task;
-        if (sM[i] == -__builtin_inff()) continue;  // a group with no pieces
-        const float sc = __builtin_amdgcn_exp2f(sM[i] - Mx);
-        num += sc * sAcc[i];
-        den += sc * sS[i];
-      }
+  const int b = (int)blockIdx.x / p.num_kv_heads, g = (int)blockIdx.x - b * p.num_kv_heads;
+  const int64_t row = (int64_t)b * p.num_q_heads + g * G + n;
+  const int4 cut = p.cuts[blockIdx.x];
+  const int Sk = p.group_shared[(p.seq0 + b) / p.group_size];
+  float M = -__builtin_inff(), S = 0.f;
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (active) {
+    float lse = -__builtin_inff();
+    f32x4 o32 = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (sg == 0) {
+      lse = p.lse[row];
+      o32 = *(const f32x4*)(p.out32 + row * D + 4 * d4);
     }
-  };
-  auto store_row = [&](int b, int g, f32x4 num, float den) {
-    const float inv = den > 0.f ? 1.f / den : 0.f;
-    const int64_t row = (int64_t)b * p.num_q_heads + g * G + n;
+    if (cut.x >= 0) {  // uniform: a cut segment's pieces
+      const int64_t wa = cut.x;
+      const int np = cut.y, first_off = cut.z;
+      for (int k0 = sg; k0 < np; k0 += groups * kCombineBatch) {
+        float2 ml[kCombineBatch];
+        f32x4 o[kCombineBatch];
+#pragma unroll
+        for (int i = 0; i < kCombineBatch; ++i) {  // all loads of the batch first
+          const int k = k0 + i * groups;
+          ml[i] = make_float2(-__builtin_inff(), 0.f);
+          o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (k < np) {
+            const int64_t r = (2 * (wa + k) + (k == 0 ? first_off : 0)) * G + n;
+            ml[i] = p.part_ml[r];
+            o[i] = *(const f32x4*)(p.part_o + r * D + 4 * d4);
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < kCombineBatch; ++i) merge_piece(ml[i], o[i], M, S, acc);
+      }
+    } else if (sg == 0) {  // finished whole by the decode
+      M = lse;
+      S = lse > -__builtin_inff() ? 1.f : 0.f;
+      acc = o32;
+    }
+    fold_prefix_chunks(p, b, g, n, d4, Sk, sg, groups, M, S, acc);
+  }
+  sM[t] = M;
+  sS[t] = S;
+  sAcc[t] = acc;
+  __syncthreads();
+  if (sg == 0 && task < tasks) {
+    float Mx = M;
+    for (int k = 1; k < groups; ++k) Mx = fmaxf(Mx, sM[k * tasks_r + task]);
+    f32x4 num = f32x4{0.f, 0.f, 0.f, 0.f};
+    float den = 0.f;
+    for (int k = 0; k < groups; ++k) {
+      const int i = k * tasks_r + task;
+      if (sM[i] == -__builtin_inff()) continue;  // a group with no pieces
+      const float sc = __builtin_amdgcn_exp2f(sM[i] - Mx);
+      num += sc * sAcc[i];
+      den += sc * sS[i];
+    }
+    const float inv = den > 0.f ? 1.f / den : 0.f;  // an empty row with no prefix is zero
     *(bf16x4*)(p.out + row * D + 4 * d4) =
         bf16x4{(__bf16)(num[0] * inv), (__bf16)(num[1] * inv), (__bf16)(num[2] * inv),
                (__bf16)(num[3] * inv)};
-  };
-  if ((int)blockIdx.x < p.waves) {
-    const int4 cut = p.cuts[blockIdx.x];
-    if (cut.x >= 0) {  // uniform
-      const int64_t wa = blockIdx.x;
-      const int b = cut.x, g = cut.y, np = cut.z, first_off = cut.w;
-      const int Sk = p.group_shared[(p.seq0 + b) / p.group_size];
-      float M = -__builtin_inff(), S = 0.f;
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (active) {
-        for (int k0 = sg; k0 < np; k0 += groups * kCombineBatch) {
-          float2 ml[kCombineBatch];
-          f32x4 o[kCombineBatch];
-#pragma unroll
-          for (int i = 0; i < kCombineBatch; ++i) {  // all loads of the batch first
-            const int k = k0 + i * groups;
-            ml[i] = make_float2(-__builtin_inff(), 0.f);
-            o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (k < np) {
-              const int64_t row = (2 * (wa + k) + (k == 0 ? first_off : 0)) * G + n;
-              ml[i] = p.part_ml[row];
-              o[i] = *(const f32x4*)(p.part_o + row * D + 4 * d4);
-            }
-          }
-#pragma unroll
-          for (int i = 0; i < kCombineBatch; ++i) merge_piece(ml[i], o[i], M, S, acc);
-        }
-        fold_prefix_chunks(p, b, g, n, d4, Sk, sg, groups, M, S, acc);
-      }
-      float Mx, den;
-      f32x4 num;
-      merge_groups(M, S, acc, Mx, den, num);
-      if (sg == 0 && task < tasks) store_row(b, g, num, den);
-    }
-  }
-  // Segment (b, g) finished whole by the decode: its normalised rows in
-  // out32 with weight 2^lse, as the first piece of thread group 0.
-  if ((int64_t)blockIdx.x < (int64_t)p.num_seqs * p.num_kv_heads) {  // uniform
-    const int b = (int)blockIdx.x / p.num_kv_heads, g = (int)blockIdx.x - b * p.num_kv_heads;
-    if (p.seg_cut[blockIdx.x] == 0) {  // uniform
-      __syncthreads();  // LDS reuse after a cut record's merge
-      const int Sk = p.group_shared[(p.seq0 + b) / p.group_size];
-      float M = -__builtin_inff(), S = 0.f;
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (active) {
-        if (sg == 0) {
-          const int64_t row = (int64_t)b * p.num_q_heads + g * G + n;
-          M = p.lse[row];
-          S = M > -__builtin_inff() ? 1.f : 0.f;
-          acc = *(const f32x4*)(p.out32 + row * D + 4 * d4);
-        }
-        fold_prefix_chunks(p, b, g, n, d4, Sk, sg, groups, M, S, acc);
-      }
-      float Mx, den;
-      f32x4 num;
-      merge_groups(M, S, acc, Mx, den, num);
-      if (sg == 0 && task < tasks) store_row(b, g, num, den);
-    }
   }
 }
 

@@ -50,32 +50,36 @@ struct DecodeParams {
   float* lse;          // with each row's base-2 log-sum-exp [B][Hq] (scores in log2 units),
   const int32_t* skip; // and sequence b starts at page skip[(skip_seq0 + b) / skip_group]
   int32_t skip_seq0, skip_group;
-  int4* cuts;          // per wavefront: {b, g, pieces, first-slot offset} or b = -1
+  int4* cuts;          // cut records, per wavefront or per segment (seg_records)
   float* part_o;
   float2* part_ml;
   int32_t num_seqs, num_q_heads, num_kv_heads, group, stride;
   int32_t min_range;   // smallest range in page-heads
   int64_t page_bytes;  // bytes of one K (or V) page, all KV heads
   float scale_log2;    // softmax scale times log2(e)
-  int32_t* seg_cut;    // with out32: [B][Hkv] 1 where the segment was cut, else 0
+  // 0: cuts[w] = {b, g, pieces, first-slot offset} of the cut segment whose
+  // first piece wavefront w holds, or b = -1.  1: cuts[b * Hkv + g] = {w,
+  // pieces, first-slot offset, 0} for a cut segment, w = -1 for a segment
+  // finished whole or empty (every segment's record is written every call).
+  int32_t seg_records;
 };
 
 struct CombineParams {
-  const int4* cuts;
+  const int4* cuts;             // as DecodeParams::cuts, with seg_records
   const float* part_o;
   const float2* part_ml;
   uint16_t* out;
   float* out32;  // if set (and not grouped): fp32 rows and their log-sum-exp
   float* lse;
   int32_t num_q_heads, group, head_dim;
-  // Grouped decode only: every row of this launch's sequences is folded with
-  // its group's prefix partials before the bf16 store.  Rows the decode
-  // finished whole come from out32 / lse; cut ones from the pieces.
-  const int32_t* seg_cut;       // [num_seqs][num_kv_heads], from the decode
+  int32_t seg_records;
+  // Grouped decode only (records per segment): every row of this launch's
+  // sequences is folded with its group's prefix partials before the bf16
+  // store.  Rows the decode finished whole come from out32 / lse; cut ones
+  // from the pieces.
   const int32_t* group_shared;  // per group: shared full pages
   const float* pre_o;           // prefix partials, as GroupedParams::part_o
   const float2* pre_ml;
-  int32_t waves;                // decode wavefronts (cut records)
   int32_t num_seqs, seq0, num_kv_heads, group_size, cmax;
   int64_t pre_kh;               // groups x KV heads of the whole batch
 };
@@ -121,11 +125,11 @@ struct GroupedParams {
 
 hipError_t launch_grouped_prefix(const GroupedParams& p, int grid, bool fp8, hipStream_t s);
 // The suffix decode of the grouped path: out32 / lse hold rows the decode
-// finishes whole, seg_cut which segments were cut; the combine then writes
-// every row to gp.out folded with the prefix partials.
+// finishes whole, seg_rec every segment's cut record; the combine then
+// writes every row to gp.out folded with the prefix partials.
 struct GroupedSuffix {
   const GroupedParams* gp;
-  int32_t* seg_cut;  // [min(B, kMaxSeqsPerLaunch)][Hkv], reused per launch
+  int4* seg_rec;  // [min(B, kMaxSeqsPerLaunch)][Hkv], reused per launch
 };
 dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void* k_pages,
                            const void* v_pages, const int32_t* block_table,

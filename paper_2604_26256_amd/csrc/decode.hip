@@ -33,11 +33,13 @@
 //            folded into the scores (K) and the probabilities (V).
 //            Each wavefront records the one cut segment whose first piece it
 //            holds (at most one: its last segment), and writes the zero output
-//            of a share of the empty sequences.
-//   combine  one workgroup per wavefront: the log-sum-exp merge of the pieces
-//            of the cut segment that wavefront recorded.  The grouped
-//            decode's variant also folds every row with the partials of its
-//            group's shared prefix.
+//            of a share of the empty sequences.  When the batch has no more
+//            segments than wavefronts the records are kept per segment
+//            instead (every segment's record written every call).
+//   combine  one workgroup per record: the log-sum-exp merge of the pieces
+//            of a cut segment.  The grouped decode's variant has one
+//            workgroup per segment and also folds every row with the
+//            partials of its group's shared prefix.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 

@@ -502,14 +502,9 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(CombineParams 
     }
     const float inv = 1.f / den;
     const int64_t row = (int64_t)b * p.num_q_heads + g * G + n;
-    if (p.out32) {
-      *(f32x4*)(p.out32 + row * D + 4 * d4) = num * inv;
-      if (d4 == 0) p.lse[row] = Mx + __builtin_amdgcn_logf(den);
-    } else {
-      uint16_t* o = p.out + row * D + 4 * d4;
-      *(bf16x4*)o = bf16x4{(__bf16)(num[0] * inv), (__bf16)(num[1] * inv),
-                           (__bf16)(num[2] * inv), (__bf16)(num[3] * inv)};
-    }
+    uint16_t* o = p.out + row * D + 4 * d4;
+    *(bf16x4*)o = bf16x4{(__bf16)(num[0] * inv), (__bf16)(num[1] * inv),
+                         (__bf16)(num[2] * inv), (__bf16)(num[3] * inv)};
   }
 }
 

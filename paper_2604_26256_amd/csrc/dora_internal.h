@@ -46,8 +46,8 @@ struct DecodeParams {
   const int32_t* block_table;
   const int32_t* seq_lens;
   uint16_t* out;
-  float* out32;        // if set: normalised fp32 output [B][Hq][d] instead of `out`,
-  float* lse;          // with each row's base-2 log-sum-exp [B][Hq] (scores in log2 units),
+  float* out32;        // grouped suffix: normalised fp32 rows [B][Hq][d] of the segments
+  float* lse;          // finished whole (not `out`), their base-2 log-sum-exp [B][Hq],
   const int32_t* skip; // and sequence b starts at page skip[(skip_seq0 + b) / skip_group]
   int32_t skip_seq0, skip_group;
   int4* cuts;          // cut records, per wavefront or per segment (seg_records)
@@ -68,15 +68,15 @@ struct CombineParams {
   const int4* cuts;             // as DecodeParams::cuts, with seg_records
   const float* part_o;
   const float2* part_ml;
-  uint16_t* out;
-  float* out32;  // if set (and not grouped): fp32 rows and their log-sum-exp
-  float* lse;
+  uint16_t* out;                // bf16 rows of this launch's sequences
   int32_t num_q_heads, group, head_dim;
   int32_t seg_records;
   // Grouped decode only (records per segment): every row of this launch's
   // sequences is folded with its group's prefix partials before the bf16
   // store.  Rows the decode finished whole come from out32 / lse; cut ones
   // from the pieces.
+  const float* out32;
+  const float* lse;
   const int32_t* group_shared;  // per group: shared full pages
   const float* pre_o;           // prefix partials, as GroupedParams::part_o
   const float2* pre_ml;

@@ -32,36 +32,56 @@ constexpr int NCW = 1;         // column tiles per computing wave (2 measured no
 // Shared prefix of group k (all threads of the workgroup get it): the number
 // of leading pages that every member holds in full (floor(len / P), at most
 // the table's width) and whose page id equals the leader's; a group of one
-// shares nothing.  Returns early, with a value <= `enough`, once every member's
-// full pages number at most `enough`.
+// shares nothing.  Returns early, with a value <= `enough`, once every
+// member's full pages number at most `enough`.
+//   The loads of the common case (at most kDetectBatch members) issue at
+// once, so that the detection costs one round trip: each thread reads the
+// members' lengths itself (the same few lines for all threads: the cap needs
+// no barrier and no atomics), then the entries j = threadIdx.x of every
+// member's row (entries past a member's pages are read and ignored: the rows
+// are stride wide).  The lengths go first, so a workgroup whose chunk lies
+// past the cap leaves as soon as they arrive.  More members, and prefixes
+// longer than the workgroup, are compared in further passes.
+constexpr int kDetectBatch = 16;
+template <int P>
 __device__ int shared_prefix(const GroupedParams& p, int k, int enough) {
-  __shared__ int s_cap, s_min;
-  const int M = p.group_size, P = p.page_size, stride = p.stride;
+  __shared__ int s_min;
+  const int M = p.group_size, stride = p.stride;
   const int64_t b0 = (int64_t)k * M;
   if (M == 1) return 0;
-  int L = 0;  // issued before the first barrier: its latency overlaps the waves' start
-  if ((int)threadIdx.x < M) L = p.seq_lens[b0 + threadIdx.x];
-  if (threadIdx.x == 0) s_cap = s_min = stride;
-  __syncthreads();
-  if ((int)threadIdx.x < M) atomicMin(&s_cap, L > 0 ? L / P : 0);
-  __syncthreads();
-  const int cap = s_cap;  // final here; mismatches go to s_min
-  if (cap <= enough) return cap;
-  // Thread j holds the leader's entry j and compares it with every member's;
-  // the member loads are independent, so they issue back to back (no
-  // division, no atomics inside the loops).
   const int32_t* __restrict__ bt = p.block_table + b0 * stride;
-  int first = cap;  // this thread's smallest mismatch
-  for (int j = threadIdx.x; j < cap; j += blockDim.x) {
-    const int32_t lead = bt[j];
-    bool diff = false;
-#pragma unroll 8
-    for (int m = 1; m < M; ++m) diff |= bt[(int64_t)m * stride + j] != lead;
-    if (diff && j < first) first = j;
+  const int j = (int)threadIdx.x < stride ? (int)threadIdx.x : stride - 1;
+  int L[kDetectBatch];
+  int32_t e[kDetectBatch];
+#pragma unroll
+  for (int i = 0; i < kDetectBatch; ++i) L[i] = p.seq_lens[b0 + (i < M ? i : M - 1)];
+  const int32_t lead = bt[j];
+#pragma unroll
+  for (int i = 0; i < kDetectBatch; ++i) e[i] = bt[(int64_t)(i < M ? i : M - 1) * stride + j];
+  int cap = stride;
+#pragma unroll
+  for (int i = 0; i < kDetectBatch; ++i) cap = min(cap, L[i] > 0 ? L[i] / P : 0);
+  for (int m = kDetectBatch; m < M; ++m) {
+    const int Lm = p.seq_lens[b0 + m];
+    cap = min(cap, Lm > 0 ? Lm / P : 0);
+  }
+  if (cap <= enough) return cap;  // uniform: every thread read the same lengths
+  bool diff = false;
+#pragma unroll
+  for (int i = 0; i < kDetectBatch; ++i) diff |= e[i] != lead;
+  for (int m = kDetectBatch; m < M; ++m) diff |= bt[(int64_t)m * stride + j] != lead;
+  if (threadIdx.x == 0) s_min = cap;
+  __syncthreads();
+  int first = diff && (int)threadIdx.x < cap ? (int)threadIdx.x : cap;  // smallest mismatch
+  for (int jj = threadIdx.x + blockDim.x; jj < cap; jj += blockDim.x) {
+    const int32_t ld = bt[jj];
+    bool d = false;
+    for (int m = 1; m < M; ++m) d |= bt[(int64_t)m * stride + jj] != ld;
+    if (d && jj < first) first = jj;
   }
   if (first < cap) atomicMin(&s_min, first);
   __syncthreads();
-  return s_min < cap ? s_min : cap;
+  return s_min;
 }
 
 // The split of a group's shared pages into work items: prefix_chunk_of.
@@ -118,7 +138,7 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(GroupedParams p)
   // The group's shared prefix; the first workgroup of each group publishes it
   // for the suffix decode and its combine.  A chunk that starts past every
   // member's full pages has no work whatever the prefix is.
-  const int S = shared_prefix(p, k, c * kPrefixMinChunk);
+  const int S = shared_prefix<P>(p, k, c * kPrefixMinChunk);
   if (c == 0 && g == 0 && threadIdx.x == 0) {
     p.group_shared[k] = S;
     if (p.shared_out) p.shared_out[k] = S;

@@ -554,7 +554,8 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
-              "(the decode path shards by sequence with no exchange; see DESIGN.md)",
+              "(one GPU's share is measured; the decode path would shard by sequence with "
+              "no exchange between GPUs)",
               file=sys.stderr)
         sys.exit(2)
     import torch

@@ -131,9 +131,11 @@ const char* dora_status_string(dora_status s);
 
 /* Bytes of device workspace dora_decode_attn needs for this geometry on the
  * current device (valid for every seq_lens the call may see).  Returns 0 for an
- * invalid or unsupported descriptor.  The workspace holds the batch's page
- * prefix and two partial results per decode wavefront (unnormalised output,
- * running max and sum in fp32). */
+ * invalid or unsupported descriptor.  The workspace holds a 256-byte flag
+ * header, one cut record per decode wavefront (or per (sequence, KV head)
+ * segment, when there are no more segments than wavefronts) and two partial
+ * results per wavefront (unnormalised output, running max and sum in fp32);
+ * the batch's page prefix is built in each wavefront's LDS. */
 size_t dora_decode_workspace_bytes(const dora_decode_desc* desc);
 
 /* Decode-step attention over the paged, multi-version KV pool (the operation

@@ -179,6 +179,36 @@ def test_validate_flag_accepts_good_and_rejects_bad_pages():
     assert e.value.status == d.DORA_ERR_DEVICE_CHECK
 
 
+
+@pytest.mark.parametrize("bad", ["len_past_table", "len_negative", "page_negative"])
+def test_validate_flag_rejects_bad_lengths_and_ids(bad):
+    """DORA_FLAG_VALIDATE also rejects a length the block table cannot hold,
+    a negative length and a negative page id, before any decode launch (the
+    output keeps its sentinel), and a good call right after passes (the
+    check's flag is cleared on every call)."""
+    print(f"[case] validate {bad}", flush=True)
+    lens = np.array([40, 300, 17, 129], np.int32)
+    w = _w(B=len(lens), Hq=8, Hkv=2, d=64, P=16, dt=0, lens=lens)
+    b = gpu_batch(w, lengths=lens, seed_index=9)
+    d = lib()
+    good_bt, good_lens = b.block_table.clone(), b.seq_lens.clone()
+    stride = b.block_table.shape[1]
+    if bad == "len_past_table":
+        b.seq_lens[1] = stride * w.page_size + 1
+    elif bad == "len_negative":
+        b.seq_lens[2] = -1
+    else:
+        b.block_table[3, 2] = -3
+    sentinel = torch.full_like(b.q, 7.0)
+    out = sentinel.clone()
+    with pytest.raises(d.DoraError) as e:
+        run_decode(b, out=out, flags=d.DORA_FLAG_VALIDATE)
+    assert e.value.status == d.DORA_ERR_DEVICE_CHECK
+    assert torch.equal(out, sentinel)
+    b.block_table, b.seq_lens = good_bt, good_lens
+    out = run_decode(b, flags=d.DORA_FLAG_VALIDATE)
+    assert max_abs_err(out, oracle_for(b)) <= TOL[0]
+
 def test_empty_batch_is_a_no_op():
     d = lib()
     q = torch.empty((0, 8, 64), dtype=torch.bfloat16, device="cuda")

@@ -120,10 +120,6 @@ typedef struct {
                                   minimum range) */
   int32_t min_range_pages;     /* smallest work range per wavefront, in
                                   (page, KV head) units; 0 = library default */
-  void**  prof_events;         /* NULL, or 3 caller-created hipEvent_t recorded on
-                                  `stream` before the decode kernel, between it
-                                  and the combine kernel, and after the combine
-                                  kernel (per-kernel timing) */
 } dora_decode_desc;
 
 /* Human-readable name of a status code (static storage). */
@@ -137,6 +133,17 @@ const char* dora_status_string(dora_status s);
  * results per wavefront (unnormalised output, running max and sum in fp32);
  * the batch's page prefix is built in each wavefront's LDS. */
 size_t dora_decode_workspace_bytes(const dora_decode_desc* desc);
+
+/* Decode wavefronts dora_decode_attn launches per launch for this descriptor on
+ * the current device: desc->num_waves when it is set, else the library default
+ * described at dora_decode_desc.num_waves.  Wavefront w takes page-heads
+ * [w*T/W', (w+1)*T/W') of the launch's T (sequence, KV head, page) work items
+ * in (sequence, head, page) order, where W' = min(W, ceil(T / m)), m being
+ * desc->min_range_pages or 8 when that is 0, and the first T mod W' ranges hold
+ * one extra item; so a caller can tell which (sequence, KV head) segments a
+ * call cuts across wavefronts.  Each launch covers at most 8192 sequences.
+ * Returns 0 for an invalid or unsupported descriptor. */
+int64_t dora_decode_num_waves(const dora_decode_desc* desc);
 
 /* Decode-step attention over the paged, multi-version KV pool (the operation
  * defined at the top of this file; the step the paper times as tau per output

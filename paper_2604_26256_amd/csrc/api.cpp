@@ -118,6 +118,11 @@ size_t dora_decode_workspace_bytes(const dora_decode_desc* desc) {
   return w.total;
 }
 
+int64_t dora_decode_num_waves(const dora_decode_desc* desc) {
+  if (check_desc(desc) != DORA_OK) return 0;
+  return decode_waves(*desc);
+}
+
 }  // extern "C"
 
 namespace dora {
@@ -274,14 +279,11 @@ dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void*
   return DORA_OK;
 }
 
-}  // namespace dora
-
-extern "C" {
-
-dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const void* k_pages,
-                             const void* v_pages, const int32_t* block_table,
-                             const int32_t* seq_lens, const int32_t* version_ids, void* out,
-                             void* workspace, size_t workspace_bytes, dora_stream_t stream) {
+// dora_decode_attn with optional timing events (ev: NULL or three events).
+dora_status decode_attn(const dora_decode_desc* desc, const void* q, const void* k_pages,
+                        const void* v_pages, const int32_t* block_table, const int32_t* seq_lens,
+                        const int32_t* version_ids, void* out, void* workspace,
+                        size_t workspace_bytes, hipStream_t s, hipEvent_t* ev) {
   dora_status st = check_desc(desc);
   if (st != DORA_OK) return st;
   const dora_decode_desc& d = *desc;
@@ -299,10 +301,7 @@ dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const 
   ws_layout(d, decode_waves(d), &w);
   if (workspace_bytes < w.total) return DORA_ERR_WORKSPACE_TOO_SMALL;
 
-  hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace;
-  hipEvent_t* ev = (hipEvent_t*)d.prof_events;
-
   if (validate) {
     st = validate_tables(d, block_table, seq_lens, version_ids, (int32_t*)ws, s);
     if (st != DORA_OK) return st;
@@ -310,6 +309,18 @@ dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const 
 
   return enqueue_decode(d, q, k_pages, v_pages, block_table, seq_lens, (uint16_t*)out, nullptr,
                         ws, w, s, ev);
+}
+
+}  // namespace dora
+
+extern "C" {
+
+dora_status dora_decode_attn(const dora_decode_desc* desc, const void* q, const void* k_pages,
+                             const void* v_pages, const int32_t* block_table,
+                             const int32_t* seq_lens, const int32_t* version_ids, void* out,
+                             void* workspace, size_t workspace_bytes, dora_stream_t stream) {
+  return decode_attn(desc, q, k_pages, v_pages, block_table, seq_lens, version_ids, out,
+                     workspace, workspace_bytes, (hipStream_t)stream, nullptr);
 }
 
 size_t dora_decode_grouped_workspace_bytes(const dora_decode_desc* desc, int32_t group_size) {

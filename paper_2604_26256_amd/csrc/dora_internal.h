@@ -135,6 +135,12 @@ dora_status enqueue_decode(const dora_decode_desc& d, const void* q, const void*
                            const void* v_pages, const int32_t* block_table,
                            const int32_t* seq_lens, uint16_t* out, const GroupedSuffix* gs,
                            uint8_t* ws, const WsLayout& w, hipStream_t s, hipEvent_t* ev);
+// dora_decode_attn, with three timing events recorded on `s` when ev is set:
+// before the first decode kernel, after it, and after the last combine kernel.
+dora_status decode_attn(const dora_decode_desc* desc, const void* q, const void* k_pages,
+                        const void* v_pages, const int32_t* block_table, const int32_t* seq_lens,
+                        const int32_t* version_ids, void* out, void* workspace,
+                        size_t workspace_bytes, hipStream_t s, hipEvent_t* ev);
 
 struct ValidateParams {
   const int32_t* block_table;

@@ -48,7 +48,7 @@ class dora_decode_desc(ctypes.Structure):
         ("sm_scale", ctypes.c_float), ("k_scales", ctypes.c_void_p),
         ("v_scales", ctypes.c_void_p), ("page_owner", ctypes.c_void_p),
         ("flags", ctypes.c_uint32), ("num_waves", ctypes.c_int32),
-        ("min_range_pages", ctypes.c_int32), ("prof_events", ctypes.c_void_p),
+        ("min_range_pages", ctypes.c_int32),
     ]
 
 
@@ -73,6 +73,12 @@ _lib.dora_status_string.argtypes = [ctypes.c_int]
 _lib.dora_status_string.restype = ctypes.c_char_p
 _lib.dora_decode_workspace_bytes.argtypes = [_DescP]
 _lib.dora_decode_workspace_bytes.restype = _SZ
+_lib.dora_decode_num_waves.argtypes = [_DescP]
+_lib.dora_decode_num_waves.restype = _I64
+_lib.dora_decode_attn_timed.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P]
+_lib.dora_decode_attn_timed.restype = ctypes.c_int
+_lib.dora_stream_read.argtypes = [_P, _I64, _P, _I64, _I32, _P, _I32, _P]
+_lib.dora_stream_read.restype = ctypes.c_int
 _lib.dora_decode_attn.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
 _lib.dora_decode_attn.restype = ctypes.c_int
 _lib.dora_decode_grouped_workspace_bytes.argtypes = [_DescP, _I32]
@@ -207,7 +213,7 @@ def _kv_geometry(k_pages, v_pages, num_kv_heads, page_size, head_dim, kv_dtype):
 def make_decode_desc(*, num_seqs, num_q_heads, num_kv_heads, head_dim, page_size,
                      block_table_stride, num_pages, kv_dtype=DORA_KV_BF16, sm_scale=0.0,
                      k_scales=None, v_scales=None, page_owner=None, flags=0, num_waves=0,
-                     min_range_pages=0, prof_events=None) -> dora_decode_desc:
+                     min_range_pages=0) -> dora_decode_desc:
     d = dora_decode_desc()
     d.num_seqs, d.num_q_heads, d.num_kv_heads = num_seqs, num_q_heads, num_kv_heads
     d.head_dim, d.page_size, d.block_table_stride = head_dim, page_size, block_table_stride
@@ -216,7 +222,6 @@ def make_decode_desc(*, num_seqs, num_q_heads, num_kv_heads, head_dim, page_size
     d.v_scales = None if v_scales is None else v_scales.data_ptr()
     d.page_owner = None if page_owner is None else page_owner.data_ptr()
     d.flags, d.num_waves, d.min_range_pages = flags, num_waves, min_range_pages
-    d.prof_events = prof_events
     return d
 
 
@@ -229,45 +234,48 @@ def dora_decode_grouped_workspace_bytes(desc: dora_decode_desc, group_size) -> i
     return int(_lib.dora_decode_grouped_workspace_bytes(ctypes.byref(desc), int(group_size)))
 
 
+def dora_decode_num_waves(desc: dora_decode_desc) -> int:
+    """Decode wavefronts per launch for this descriptor on the current device."""
+    return int(_lib.dora_decode_num_waves(ctypes.byref(desc)))
+
+
+# Workspaces the binding allocates when the caller passes none: one per
+# (device, stream), allocated on that stream (so the caching allocator orders
+# its reuse after the stream's pending work), and replaced when a call needs a
+# different size.  Calls on different streams never share one.
 _ws_cache = {}
 
 
-def dora_decode_attn(q, k_pages, v_pages, block_table, seq_lens, version_ids, out, *,
-                     num_kv_heads: int, page_size: int, kv_dtype: int = DORA_KV_BF16,
-                     sm_scale: float = 0.0, k_scales=None, v_scales=None, page_owner=None,
-                     flags: int = 0, num_waves: int = 0, min_range_pages: int = 0,
-                     workspace=None, stream=None, prof_events=None):
-    """Decode-step attention over the paged pool (see include/dora.h).
+def _cached_workspace(cache, device, stream, need):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    key = (device.index, s.cuda_stream)
+    ws = cache.get(key)
+    if ws is None or ws.numel() != need:
+        cache.pop(key, None)
+        with torch.cuda.stream(s):
+            ws = torch.empty(need, dtype=torch.uint8, device=device)
+        cache[key] = ws
+    return ws
 
-    q, out: bf16 [B][Hq][d]; k_pages: [num_pages][Hkv][d/X][P][X]; v_pages:
-    [num_pages][Hkv][d][P] (bf16, or uint8 / float8_e4m3fn codes with fp32
-    k_scales / v_scales [num_pages]); block_table int32 [B][stride]; seq_lens,
-    version_ids int32 [B].  num_waves / min_range_pages override how the
-    work is cut (0 = library default).  prof_events: 3 raw hipEvent_t handles.
-    The workspace is allocated (and cached per device and size) when not
-    given.  Returns `out`.
-    """
+
+def _decode_args(q, k_pages, v_pages, block_table, seq_lens, version_ids, out, *, num_kv_heads,
+                 page_size, kv_dtype, sm_scale, k_scales, v_scales, page_owner, flags,
+                 num_waves, min_range_pages):
     torch = _torch()
     B, Hq, D = (int(x) for x in q.shape)
     num_pages, kv_types = _kv_geometry(k_pages, v_pages, num_kv_heads, page_size, D, kv_dtype)
     if block_table.dim() != 2 or block_table.shape[0] != B:
         raise ValueError("block_table must be [B][stride]")
     stride = int(block_table.shape[1])
-    if prof_events is not None:
-        if len(prof_events) != 3:
-            raise ValueError("prof_events needs 3 event handles")
-        arr = (ctypes.c_void_p * 3)(*[ctypes.c_void_p(e) for e in prof_events])
-        ev_ptr = ctypes.cast(arr, ctypes.c_void_p)
-    else:
-        arr, ev_ptr = None, None
     desc = make_decode_desc(num_seqs=B, num_q_heads=Hq, num_kv_heads=num_kv_heads, head_dim=D,
                             page_size=page_size, block_table_stride=max(1, stride),
                             num_pages=num_pages, kv_dtype=kv_dtype, sm_scale=sm_scale,
                             k_scales=k_scales, v_scales=v_scales, page_owner=page_owner,
                             flags=flags, num_waves=num_waves,
-                            min_range_pages=min_range_pages, prof_events=ev_ptr)
+                            min_range_pages=min_range_pages)
     if B == 0:
-        return out
+        return desc, None
     args = [
         _dev_ptr(q, "q", (torch.bfloat16,), shape=(B, Hq, D)),
         _dev_ptr(k_pages, "k_pages", kv_types),
@@ -282,24 +290,67 @@ def dora_decode_attn(q, k_pages, v_pages, block_table, seq_lens, version_ids, ou
         _dev_ptr(v_scales, "v_scales", (torch.float32,), shape=(num_pages,), align=4)
     if page_owner is not None:
         _dev_ptr(page_owner, "page_owner", (torch.int16,), shape=(num_pages,), align=2)
+    return desc, args
+
+
+def dora_decode_attn(q, k_pages, v_pages, block_table, seq_lens, version_ids, out, *,
+                     num_kv_heads: int, page_size: int, kv_dtype: int = DORA_KV_BF16,
+                     sm_scale: float = 0.0, k_scales=None, v_scales=None, page_owner=None,
+                     flags: int = 0, num_waves: int = 0, min_range_pages: int = 0,
+                     workspace=None, stream=None, events=None):
+    """Decode-step attention over the paged pool (see include/dora.h).
+
+    q, out: bf16 [B][Hq][d]; k_pages: [num_pages][Hkv][d/X][P][X]; v_pages:
+    [num_pages][Hkv][d][P] (bf16, or uint8 / float8_e4m3fn codes with fp32
+    k_scales / v_scales [num_pages]); block_table int32 [B][stride]; seq_lens,
+    version_ids int32 [B].  num_waves / min_range_pages override how the
+    work is cut (0 = library default).  stream: a torch stream (default: the
+    current one).  The workspace is allocated when not given (cached per
+    device and stream).  events: three raw hipEvent_t handles, which selects
+    dora_decode_attn_timed (include/dora_measure.h).  Returns `out`.
+    """
+    desc, args = _decode_args(q, k_pages, v_pages, block_table, seq_lens, version_ids, out,
+                              num_kv_heads=num_kv_heads, page_size=page_size,
+                              kv_dtype=kv_dtype, sm_scale=sm_scale, k_scales=k_scales,
+                              v_scales=v_scales, page_owner=page_owner, flags=flags,
+                              num_waves=num_waves, min_range_pages=min_range_pages)
+    if args is None:
+        return out
     need = dora_decode_workspace_bytes(desc)
     if need == 0:
         # invalid or unsupported geometry: let the library name the reason
         _check(_lib.dora_decode_attn(ctypes.byref(desc), *args, None, 0,
                                      _stream_handle(stream)), "dora_decode_attn")
     if workspace is None:
-        key = (q.device.index, need)
-        workspace = _ws_cache.get(key)
-        if workspace is None:
-            _ws_cache.clear()
-            workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
-            _ws_cache[key] = workspace
-    ws_ptr = _dev_ptr(workspace, "workspace", (torch.uint8,))
-    st = _lib.dora_decode_attn(ctypes.byref(desc), *args, ws_ptr, workspace.numel(),
-                               _stream_handle(stream))
-    del arr
-    _check(st, "dora_decode_attn")
+        workspace = _cached_workspace(_ws_cache, q.device, stream, need)
+    ws_ptr = _dev_ptr(workspace, "workspace", (_torch().uint8,))
+    if events is None:
+        st = _lib.dora_decode_attn(ctypes.byref(desc), *args, ws_ptr, workspace.numel(),
+                                   _stream_handle(stream))
+        _check(st, "dora_decode_attn")
+    else:
+        if len(events) != 3:
+            raise ValueError("events needs 3 hipEvent_t handles")
+        arr = (ctypes.c_void_p * 3)(*[ctypes.c_void_p(e) for e in events])
+        st = _lib.dora_decode_attn_timed(ctypes.byref(desc), *args, ws_ptr, workspace.numel(),
+                                         _stream_handle(stream), ctypes.cast(arr, _P))
+        _check(st, "dora_decode_attn_timed")
     return out
+
+
+def dora_stream_read(base, tiles, sink, *, tile_bytes=4096, stream=None):
+    """Streaming-read reference (include/dora_measure.h): read the tiles of
+    `base` (device uint8) listed in `tiles` (device int32) with non-temporal
+    loads, one wavefront per entry of `sink` (device int32/uint32 words)."""
+    torch = _torch()
+    n = int(tiles.numel())
+    st = _lib.dora_stream_read(
+        _dev_ptr(base, "base", (torch.uint8,)), base.numel(),
+        _dev_ptr(tiles, "tiles", (torch.int32,), numel=n, align=4) if n else None, n,
+        int(tile_bytes), _dev_ptr(sink, "sink", (torch.int32, torch.uint32), align=4),
+        int(sink.numel()), _stream_handle(stream))
+    _check(st, "dora_stream_read")
+    return sink
 
 
 _gws_cache = {}
@@ -348,12 +399,7 @@ def dora_decode_attn_grouped(q, k_pages, v_pages, block_table, seq_lens, version
                                              _stream_handle(stream)),
                "dora_decode_attn_grouped")
     if workspace is None:
-        key = (q.device.index, need)
-        workspace = _gws_cache.get(key)
-        if workspace is None:
-            _gws_cache.clear()
-            workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
-            _gws_cache[key] = workspace
+        workspace = _cached_workspace(_gws_cache, q.device, stream, need)
     st = _lib.dora_decode_attn_grouped(ctypes.byref(desc), *args,
                                        _dev_ptr(workspace, "workspace", (torch.uint8,)),
                                        workspace.numel(), _stream_handle(stream))

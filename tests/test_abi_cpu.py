@@ -11,7 +11,9 @@ import pytest
 import oracle
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "dora.h")
+HEADERS = [os.path.join(ROOT, "include", f) for f in sorted(os.listdir(os.path.join(ROOT,
+                                                                                "include")))
+           if f.endswith(".h")]
 
 
 @pytest.fixture(scope="module")
@@ -24,14 +26,19 @@ def d():
 
 
 def _declared_functions():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(dora_[a-z0-9_]+)\s*\(", src)))
+    names = set()
+    for h in HEADERS:
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names.update(re.findall(r"\b(dora_[a-z0-9_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_exports_every_declared_symbol(d):
+    assert len(HEADERS) >= 2, HEADERS
     names = _declared_functions()
-    assert len(names) >= 17, names
+    assert len(names) >= 20, names
+    for n in ("dora_decode_num_waves", "dora_decode_attn_timed", "dora_stream_read"):
+        assert n in names
     lib = d.library()
     missing = [n for n in names if not hasattr(lib, n)]
     assert not missing, missing
@@ -238,3 +245,43 @@ def test_pool_migration_rules(d):
     assert list(sp) == list(src.seq_pages(s)) and list(dp) == list(dst.seq_pages(nid))
     assert dst.seq_info(nid) == (300, 1, 19) and dst.stats(1)[0] == 19
     assert (dst.page_owner()[dp] == 1).all()
+
+
+def test_num_waves_query(d):
+    """The wave count the workspace is sized for: the caller's num_waves when
+    set; otherwise no more than the batch can use (B * Hkv * stride page-heads
+    over the 8-page minimum range) and at most 5 per CU for bf16 pages (with
+    no device here the library assumes 256 CUs at 8 waves each)."""
+    assert d.dora_decode_num_waves(_desc(d, num_waves=77)) == 77
+    small = _desc(d, num_seqs=2, num_kv_heads=2, num_q_heads=4, block_table_stride=8)
+    assert d.dora_decode_num_waves(small) == 2 * 2 * 8 // 8
+    assert d.dora_decode_num_waves(_desc(d, min_range_pages=1, num_seqs=2, num_kv_heads=2,
+                                         num_q_heads=4, block_table_stride=8)) == 32
+    big = d.dora_decode_num_waves(_desc(d, num_seqs=4000))
+    assert 0 < big <= 256 * 5
+    assert d.dora_decode_num_waves(_desc(d, num_seqs=4000, kv_dtype=1)) >= big
+    assert d.dora_decode_num_waves(_desc(d, head_dim=96)) == 0
+
+
+def test_measure_entry_points_reject_bad_arguments(d):
+    P = ctypes.c_void_p
+    lib = d.library()
+    desc = _desc(d)
+    ev = (P * 3)(FAKE, FAKE, None)
+    args = [P(FAKE)] * 7 + [P(FAKE), 1 << 30, None]
+    assert lib.dora_decode_attn_timed(ctypes.byref(desc), *args, None) == d.DORA_ERR_INVALID_ARG
+    assert lib.dora_decode_attn_timed(ctypes.byref(desc), *args,
+                                      ctypes.cast(ev, P)) == d.DORA_ERR_INVALID_ARG
+    bad = _desc(d, head_dim=96)
+    ev_ok = (P * 3)(FAKE, FAKE, FAKE)
+    assert lib.dora_decode_attn_timed(ctypes.byref(bad), *args,
+                                      ctypes.cast(ev_ok, P)) == d.DORA_ERR_UNSUPPORTED
+    sr = lib.dora_stream_read
+    assert sr(None, 1 << 20, P(FAKE), 4, 4096, P(FAKE), 8, None) == d.DORA_ERR_INVALID_ARG
+    assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 4096, None, 8, None) == d.DORA_ERR_INVALID_ARG
+    assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 4096, P(FAKE), 0, None) == d.DORA_ERR_INVALID_ARG
+    assert sr(P(FAKE + 4), 1 << 20, P(FAKE), 4, 4096, P(FAKE), 8, None) == \
+        d.DORA_ERR_INVALID_ARG
+    assert sr(P(FAKE), 1 << 20, None, 4, 4096, P(FAKE), 8, None) == d.DORA_ERR_INVALID_ARG
+    assert sr(P(FAKE), 1 << 20, P(FAKE), -1, 4096, P(FAKE), 8, None) == d.DORA_ERR_INVALID_ARG
+    assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 3072, P(FAKE), 8, None) == d.DORA_ERR_UNSUPPORTED

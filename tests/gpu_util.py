@@ -62,3 +62,57 @@ def sample_seqs(lengths: np.ndarray, k: int, seed: int):
     if rest:
         pick.update(int(x) for x in rng.choice(rest, size=min(k, len(rest)), replace=False))
     return sorted(pick)
+
+
+def decode_waves(b: wl.Batch, **kw) -> int:
+    """Wavefronts the library launches for b's decode (dora_decode_num_waves)."""
+    d = lib()
+    desc = d.make_decode_desc(num_seqs=b.w.num_seqs, num_q_heads=b.w.num_q_heads,
+                              num_kv_heads=b.w.num_kv_heads, head_dim=b.w.head_dim,
+                              page_size=b.w.page_size, block_table_stride=b.stride,
+                              num_pages=b.w.num_pages, kv_dtype=b.w.kv_dtype, **kw)
+    return d.dora_decode_num_waves(desc)
+
+
+def cut_segments(lengths, page_size, stride, num_kv_heads, waves, min_range=8):
+    """The (sequence, KV head) segments a launch cuts across wavefronts, from
+    the work split the header documents: T = Hkv x (pages of the batch)
+    page-heads in (sequence, head, page) order, W = min(waves, ceil(T /
+    min_range)) equal ranges, the first T mod W one longer.  Returns a sorted
+    list of (b, g)."""
+    n = np.minimum(wl.pages_needed(lengths, page_size), stride).astype(np.int64)
+    Hkv = int(num_kv_heads)
+    T = Hkv * int(n.sum())
+    if T == 0:
+        return []
+    W = min(int(waves), -(-T // min_range))
+    q, rem = divmod(T, W)
+    bounds = np.array([w * q + min(w, rem) for w in range(1, W)], np.int64)
+    # segment starts in flattened order
+    seq_start = Hkv * np.concatenate([[0], np.cumsum(n)[:-1]])
+    starts = (seq_start[:, None] + np.arange(Hkv)[None, :] * n[:, None]).reshape(-1)
+    lens = np.repeat(n, Hkv)
+    keep = lens > 0
+    starts, lens = starts[keep], lens[keep]
+    ids = np.nonzero(keep)[0]
+    k = np.searchsorted(starts, bounds, side="right") - 1
+    inside = (k >= 0) & (bounds > starts[np.maximum(k, 0)]) & \
+        (bounds < starts[np.maximum(k, 0)] + lens[np.maximum(k, 0)])
+    segs = sorted({(int(ids[i] // Hkv), int(ids[i] % Hkv)) for i in k[inside]})
+    return segs
+
+
+def page_chunks(lengths, page_size, max_pages):
+    """Consecutive runs of sequence indices holding at most max_pages pages
+    each (one sequence per run at least), to bound host copies."""
+    n = wl.pages_needed(lengths, page_size)
+    runs, cur, acc = [], [], 0
+    for i, nb in enumerate(n):
+        if cur and acc + nb > max_pages:
+            runs.append(cur)
+            cur, acc = [], 0
+        cur.append(i)
+        acc += int(nb)
+    if cur:
+        runs.append(cur)
+    return runs

@@ -120,14 +120,16 @@ def test_grouped_workspace_contents_ignored(fill):
     assert max_abs_err(out, oracle_for(b)) <= TOL[0]
 
 
-def test_grouped_full_size_grpo_batch_sampled():
+def test_grouped_full_size_grpo_batch_every_sequence():
+    """The GRPO batch the benchmark times: every sequence against the oracle
+    (each member read through its own block table) and the plain path."""
+    print("[case] grouped full-size grpo7b", flush=True)
     b, shared = wl.make_grpo_batch(device="cuda")
     out, det = _grouped(b, wl.GRPO_GROUP)
     assert det.tolist() == shared[::wl.GRPO_GROUP].tolist()
     assert torch.isfinite(out.float()).all()
     assert (out.float() - run_decode(b).float()).abs().max().item() <= TOL[0]
-    seqs = sorted(set([0, 1, 17, 63] + sample_seqs(b.lengths, 2, seed=5)))
-    assert max_abs_err(out, oracle_for(b, seqs), seqs) <= TOL[0]
+    assert max_abs_err(out, oracle_for(b)) <= TOL[0]
 
 
 def test_grouped_batch_larger_than_one_launch():

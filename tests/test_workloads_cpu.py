@@ -1,0 +1,92 @@
+"""CPU checks of the synthetic inputs and of the tests' own host logic.
+
+* The long-tailed workloads show the skew the paper reports for rollout
+  batches (p99 above ten times the median, Sec. 1 and Sec. 2.2): the drawn
+  lengths satisfy each workload's stated bound, stay inside its clip range,
+  and a first draw that already satisfies it is kept unchanged.
+* The set of (sequence, KV head) segments a decode launch cuts across
+  wavefronts, which the full-size parity tests use, equals a brute-force
+  enumeration of the documented equal-range split.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import workloads as wl
+from gpu_util import cut_segments, page_chunks
+
+
+@pytest.mark.parametrize("idx", range(len(wl.WORKLOADS)))
+def test_workload_lengths_meet_the_stated_skew(idx):
+    w = wl.WORKLOADS[idx]
+    L = wl.sample_lengths(w, wl.seeds(idx)[0])
+    assert len(L) == w.num_seqs and L.min() >= w.lo and L.max() <= w.hi
+    if w.min_p99_over_median:
+        assert wl.p99_over_median(L) > w.min_p99_over_median
+        st = wl.skew_stats(L)
+        assert st["bubble"] > 0.8      # the batch is dominated by its longest sequence
+
+
+def test_first_satisfying_draw_is_kept():
+    w = wl.BY_NAME["moe_fp8"]
+    seed = wl.seeds(wl.WORKLOADS.index(w))[0]
+    rng = np.random.default_rng(seed)
+    x = np.exp(rng.normal(math.log(w.median), w.sigma, size=w.num_seqs))
+    first = np.clip(np.rint(x), w.lo, w.hi).astype(np.int32)
+    assert wl.p99_over_median(first) > 10
+    assert np.array_equal(wl.sample_lengths(w, seed), first)
+
+
+def test_redraw_is_deterministic_and_raises_when_impossible():
+    w = wl.BY_NAME["rollout7b"]
+    seed = wl.seeds(1)[0]
+    assert np.array_equal(wl.sample_lengths(w, seed), wl.sample_lengths(w, seed))
+    impossible = wl.Workload("x", 64, 8, 2, 64, 16, 0, 1024, "lognormal", 100, 0.1, 1, 200,
+                             min_p99_over_median=10.0)
+    with pytest.raises(ValueError):
+        wl.sample_lengths(impossible, 1, max_draws=20)
+
+
+def _cut_brute(lengths, P, stride, Hkv, waves, min_range):
+    n = [min(-(-int(L) // P), stride) if L > 0 else 0 for L in lengths]
+    owner = []                       # page-head index -> (b, g)
+    for b, nb in enumerate(n):
+        for g in range(Hkv):
+            owner += [(b, g)] * nb
+    T = len(owner)
+    if T == 0:
+        return []
+    W = min(waves, -(-T // min_range))
+    q, rem = divmod(T, W)
+    rng_of = []
+    for w in range(W):
+        rng_of += [w] * (q + (1 if w < rem else 0))
+    seen = {}
+    for x, seg in enumerate(owner):
+        seen.setdefault(seg, set()).add(rng_of[x])
+    return sorted(s for s, r in seen.items() if len(r) > 1)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_cut_segments_match_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    B = int(rng.integers(1, 12))
+    P = int(rng.choice([16, 32]))
+    lengths = rng.integers(0, 400, size=B)
+    lengths[rng.random(B) < 0.2] = 0
+    stride = max(1, int(rng.integers(1, 30)))
+    Hkv = int(rng.integers(1, 5))
+    waves = int(rng.integers(1, 40))
+    mr = int(rng.choice([1, 3, 8]))
+    assert cut_segments(lengths, P, stride, Hkv, waves, mr) == \
+        _cut_brute(lengths, P, stride, Hkv, waves, mr)
+
+
+def test_page_chunks_cover_every_sequence_once():
+    L = np.array([10, 500, 3, 3000, 16, 17, 900], np.int32)
+    runs = page_chunks(L, 16, 64)
+    assert sorted(i for r in runs for i in r) == list(range(len(L)))
+    n = wl.pages_needed(L, 16)
+    for r in runs:
+        assert len(r) == 1 or n[r].sum() <= 64

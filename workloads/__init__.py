@@ -41,6 +41,7 @@ class Workload:
     hi: int = 1
     version_probs: tuple = (1.0,)
     pack_seqs: int = 0       # sequences moved by the pack/unpack measurement
+    min_p99_over_median: float = 0.0  # skew the drawn lengths must exceed (0: none)
 
     @property
     def group(self) -> int:
@@ -63,13 +64,17 @@ class Workload:
 # The five workloads.  Pool sizes where the workload leaves them open: the
 # smallest power of two >= 1.25x the worst page demand; the multi-version pool
 # is the stated 2^20 pages with page size 16 like the other bf16 workloads.
+# The long-tailed workloads must show the skew the paper reports (p99 above
+# ten times the median): their lengths are redrawn until they do.
 WORKLOADS = [
     Workload("tiny", 8, 8, 2, 64, 16, 0, 1024, "lognormal", 256, 1.0, 1, 2048),
-    Workload("rollout7b", 64, 28, 4, 128, 16, 0, 32768, "lognormal", 2048, 1.2, 64, 32768),
+    Workload("rollout7b", 64, 28, 4, 128, 16, 0, 32768, "lognormal", 2048, 1.2, 64, 32768,
+             min_p99_over_median=10.0),
     Workload("tail_only", 4, 32, 8, 128, 16, 0, 32768, "uniform", lo=32768, hi=98304),
     Workload("multi_version", 512, 64, 8, 128, 16, 0, 1 << 20, "lognormal", 1024, 1.3, 16,
-             65536, version_probs=(0.5, 0.3, 0.2), pack_seqs=32),
-    Workload("moe_fp8", 1024, 64, 8, 128, 32, 1, 1 << 19, "lognormal", 4096, 1.2, 128, 131072),
+             65536, version_probs=(0.5, 0.3, 0.2), pack_seqs=32, min_p99_over_median=10.0),
+    Workload("moe_fp8", 1024, 64, 8, 128, 32, 1, 1 << 19, "lognormal", 4096, 1.2, 128, 131072,
+             min_p99_over_median=10.0),
 ]
 BY_NAME = {w.name: w for w in WORKLOADS}
 
@@ -80,12 +85,26 @@ def seeds(index: int, n: int = 8) -> list:
     return [int(c.generate_state(1, np.uint64)[0] & 0x7FFFFFFFFFFFFFFF) for c in ss.spawn(n)]
 
 
-def sample_lengths(w: Workload, seed: int) -> np.ndarray:
+def p99_over_median(lengths) -> float:
+    a = np.asarray(lengths, dtype=np.float64)
+    med = float(np.median(a))
+    return float(np.percentile(a, 99) / med) if med > 0 else 0.0
+
+
+def sample_lengths(w: Workload, seed: int, max_draws: int = 1000) -> np.ndarray:
+    """Lengths of w's batch.  Lognormal: clip(rint(exp(N(ln median, sigma))),
+    lo, hi).  If w states a minimum p99/median, whole batches are drawn from the
+    same generator until one exceeds it (the first draw that does is kept)."""
     rng = np.random.default_rng(seed)
     if w.length_law == "uniform":
         return rng.integers(w.lo, w.hi + 1, size=w.num_seqs).astype(np.int32)
-    x = np.exp(rng.normal(math.log(w.median), w.sigma, size=w.num_seqs))
-    return np.clip(np.rint(x), w.lo, w.hi).astype(np.int32)
+    for _ in range(max_draws):
+        x = np.exp(rng.normal(math.log(w.median), w.sigma, size=w.num_seqs))
+        lengths = np.clip(np.rint(x), w.lo, w.hi).astype(np.int32)
+        if p99_over_median(lengths) > w.min_p99_over_median:
+            return lengths
+    raise ValueError(f"{w.name}: no draw in {max_draws} reaches p99/median > "
+                     f"{w.min_p99_over_median}")
 
 
 def sample_versions(w: Workload, seed: int) -> np.ndarray:
@@ -111,8 +130,7 @@ def skew_stats(lengths: Sequence[int]) -> dict:
     med = float(np.median(a))
     return {"sum": int(a.sum()), "mean": float(a.mean()), "median": med,
             "p99": float(np.percentile(a, 99)), "max": int(a.max()),
-            "p99_over_median": float(np.percentile(a, 99) / med) if med > 0 else 0.0,
-            "bubble": bubble(a)}
+            "p99_over_median": p99_over_median(a), "bubble": bubble(a)}
 
 
 def pages_needed(lengths: np.ndarray, page_size: int) -> np.ndarray:

@@ -19,6 +19,12 @@ def _host_codes(t: torch.Tensor) -> np.ndarray:
     return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
 
 
+def _raw(t: torch.Tensor) -> np.ndarray:
+    """Host copy of a device pool as raw bytes."""
+    return t.contiguous().cpu().view(torch.uint8).numpy().copy() if t.dtype != torch.uint8 \
+        else t.cpu().numpy().copy()
+
+
 def _geo(w):
     return dict(num_kv_heads=w.num_kv_heads, page_size=w.page_size, head_dim=w.head_dim,
                 kv_dtype=w.kv_dtype)
@@ -81,12 +87,24 @@ def test_offload_evict_restore_decodes_bitwise(dt):
         b.v_scales[idx] = 7.0
     # restore into free pages
     free = np.setdiff1d(np.arange(w.num_pages), b.used_pages)[:len(src)].astype(np.int32)
+    # oracle.unpack of the same host bytes into host copies of the pool as it is now
+    kp, vp = _raw(b.k_pages), _raw(b.v_pages)
+    ks = b.k_scales.cpu().numpy().copy() if dt else None
+    vs = b.v_scales.cpu().numpy().copy() if dt else None
+    assert oracle.unpack(host.numpy(), free, kp, vp, kv_dtype=dt, page_size=P,
+                         num_kv_heads=4, head_dim=128, policy_version=0, k_scales=ks,
+                         v_scales=vs) == 0
     status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
     d.dora_kv_page_unpack(host, torch.from_numpy(free).cuda(), b.k_pages, b.v_pages,
                           src_version=0, policy_version=0, k_scales=b.k_scales,
                           v_scales=b.v_scales, dev_status=status, **_geo(w))
     torch.cuda.synchronize()
     assert status.item() == d.DORA_OK
+    # the restored pool equals the oracle's byte for byte (tail slots included)
+    assert np.array_equal(_raw(b.k_pages), kp) and np.array_equal(_raw(b.v_pages), vp)
+    if dt:
+        assert np.array_equal(b.k_scales.cpu().numpy().view(np.uint32), ks.view(np.uint32))
+        assert np.array_equal(b.v_scales.cpu().numpy().view(np.uint32), vs.view(np.uint32))
     bt = b.block_table_h.copy()
     off = 0
     for i in moved:

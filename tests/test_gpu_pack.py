@@ -52,6 +52,86 @@ def test_pack_bit_exact_vs_oracle(dt):
     assert np.array_equal(got, ref)
 
 
+def _host_pool(t: torch.Tensor) -> np.ndarray:
+    """Host copy of a page pool (or scale array) as raw bytes, any dtype."""
+    t = t.detach().contiguous().cpu()
+    return t.view(torch.uint8).numpy().copy() if t.dtype != torch.uint8 else t.numpy().copy()
+
+
+def _oracle_unpack_expected(packed_host, dst_pages, k_before, v_before, ks_before, vs_before,
+                            *, dt, P, Hkv, d, version):
+    """oracle.unpack of the same packed bytes into host copies of the
+    destination pool as it was before the GPU unpack."""
+    kp, vp = k_before.copy(), v_before.copy()
+    ks = None if ks_before is None else ks_before.view(np.float32).copy()
+    vs = None if vs_before is None else vs_before.view(np.float32).copy()
+    rc = oracle.unpack(packed_host, np.asarray(dst_pages, np.int32), kp, vp, kv_dtype=dt,
+                       page_size=P, num_kv_heads=Hkv, head_dim=d, policy_version=version,
+                       k_scales=ks, v_scales=vs)
+    assert rc == 0, rc
+    return kp, vp, ks, vs
+
+
+def _assert_pools_equal_oracle(dst_k, dst_v, dst_ks, dst_vs, expected):
+    kp, vp, ks, vs = expected
+    assert np.array_equal(_host_pool(dst_k), kp), "K pool differs from oracle.unpack"
+    assert np.array_equal(_host_pool(dst_v), vp), "V pool differs from oracle.unpack"
+    if ks is not None:
+        assert np.array_equal(_host_pool(dst_ks), ks.view(np.uint8)), "k scales differ"
+        assert np.array_equal(_host_pool(dst_vs), vs.view(np.uint8)), "v scales differ"
+
+
+@pytest.mark.parametrize("where", ["device", "pinned_host"])
+@pytest.mark.parametrize("dt", [0, 1])
+def test_unpack_bit_exact_vs_oracle(dt, where):
+    """GPU unpack (from a device buffer, or from pinned host memory) equals
+    oracle.unpack of the same packed bytes, byte for byte over the whole
+    destination pool: the written pages with their tail slots (NaN-poisoned
+    at the source), the pages left alone, and the fp8 page scales."""
+    print(f"[case] unpack vs oracle dt={dt} {where}", flush=True)
+    d = lib()
+    P = 16 if dt == 0 else 32
+    lens = np.array([700, 33, 1, 130, 64], np.int32)
+    Hkv, D = 4, 128
+    w = wl.Workload("up", len(lens), 16, Hkv, D, P, dt, 512, "uniform", lo=1, hi=1)
+    b = gpu_batch(w, lengths=lens, seed_index=24 + dt)
+    n = wl.pages_needed(lens, P)
+    src = np.concatenate([b.block_table_h[i, :n[i]] for i in range(len(lens))]).astype(np.int32)
+    version = 1
+    packed = _pack(b, src, version)
+    if where == "pinned_host":
+        host = torch.empty(packed.numel(), dtype=torch.uint8, pin_memory=True)
+        host.copy_(packed.cpu())
+        packed = host
+    # destination pool: another geometry-equal pool filled with random bytes
+    g = torch.Generator(device="cuda").manual_seed(1234 + dt)
+    nb = w.num_pages
+    dst_k = torch.randint(0, 256, (b.k_pages.numel() * b.k_pages.element_size(),),
+                          generator=g, device="cuda", dtype=torch.uint8)
+    dst_v = torch.randint(0, 256, (b.v_pages.numel() * b.v_pages.element_size(),),
+                          generator=g, device="cuda", dtype=torch.uint8)
+    dst_k = dst_k.view(b.k_pages.dtype).view(b.k_pages.shape)
+    dst_v = dst_v.view(b.v_pages.dtype).view(b.v_pages.shape)
+    dst_ks = dst_vs = None
+    if dt:
+        dst_ks = torch.rand(nb, generator=g, device="cuda", dtype=torch.float32)
+        dst_vs = torch.rand(nb, generator=g, device="cuda", dtype=torch.float32)
+    dst_pages = np.random.default_rng(7 + dt).permutation(nb)[:len(src)].astype(np.int32)
+    expected = _oracle_unpack_expected(
+        _host_pool(packed), dst_pages, _host_pool(dst_k), _host_pool(dst_v),
+        None if dst_ks is None else _host_pool(dst_ks),
+        None if dst_vs is None else _host_pool(dst_vs), dt=dt, P=P, Hkv=Hkv, d=D,
+        version=version)
+    status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    d.dora_kv_page_unpack(packed, torch.from_numpy(dst_pages).cuda(), dst_k, dst_v,
+                          src_version=version, num_kv_heads=Hkv, page_size=P, head_dim=D,
+                          kv_dtype=dt, policy_version=version, k_scales=dst_ks,
+                          v_scales=dst_vs, dev_status=status)
+    torch.cuda.synchronize()
+    assert status.item() == d.DORA_OK
+    _assert_pools_equal_oracle(dst_k, dst_v, dst_ks, dst_vs, expected)
+
+
 @pytest.mark.parametrize("dt", [0, 1])
 def test_migration_preserves_decode_bitwise(dt):
     """Two same-version instances (two host pools over two device pools):
@@ -101,12 +181,19 @@ def test_migration_preserves_decode_bitwise(dt):
     for sid in ids:
         nid, sp, dp = src_pool.migrate_seq(sid, dst_pool, version)
         packed = _pack(b, sp, version)
+        # what the oracle's unpack makes of the same bytes and the same pool
+        expected = _oracle_unpack_expected(
+            _host_pool(packed), dp, _host_pool(dst_k), _host_pool(dst_v),
+            None if dst_ks is None else _host_pool(dst_ks),
+            None if dst_vs is None else _host_pool(dst_vs), dt=dt, P=P, Hkv=4, d=128,
+            version=version)
         d.dora_kv_page_unpack(packed, torch.from_numpy(dp).cuda(), dst_k, dst_v,
                               src_version=version, num_kv_heads=4, page_size=P, head_dim=128,
                               kv_dtype=dt, policy_version=version, k_scales=dst_ks,
                               v_scales=dst_vs, dev_status=status)
         torch.cuda.synchronize()
         assert status.item() == d.DORA_OK
+        _assert_pools_equal_oracle(dst_k, dst_v, dst_ks, dst_vs, expected)
         src_pool.free_seq(sid)
         new_ids.append(nid)
     bt2, lens2, vers2 = dst_pool.block_table(new_ids, stride=bt.shape[1])
@@ -172,5 +259,23 @@ def test_pack_multi_version_workload_32_seqs():
     got = packed.cpu().numpy()
     # the oracle saw a compacted pool holding the same pages; the buffers match whole
     assert np.array_equal(got, ref)
-    del b
+    # unpack the set into a fresh destination pool of its own (the full pool is
+    # 64 GiB, too large to compare on the host), at scattered pages, against
+    # oracle.unpack of the same bytes
+    nd = len(src) + 1024
+    dst_k = torch.full((nd,) + tuple(b.k_pages.shape[1:]), 3.0, dtype=b.k_pages.dtype,
+                       device="cuda")
+    dst_v = torch.full((nd,) + tuple(b.v_pages.shape[1:]), -5.0, dtype=b.v_pages.dtype,
+                       device="cuda")
+    dst_pages = np.random.default_rng(8).permutation(nd)[:len(src)].astype(np.int32)
+    expected = _oracle_unpack_expected(ref, dst_pages, _host_pool(dst_k), _host_pool(dst_v),
+                                       None, None, dt=0, P=16, Hkv=8, d=128, version=version)
+    status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    lib().dora_kv_page_unpack(packed, torch.from_numpy(dst_pages).cuda(), dst_k, dst_v,
+                              src_version=version, num_kv_heads=8, page_size=16, head_dim=128,
+                              policy_version=version, dev_status=status)
+    torch.cuda.synchronize()
+    assert status.item() == 0
+    _assert_pools_equal_oracle(dst_k, dst_v, None, None, expected)
+    del b, dst_k, dst_v
     torch.cuda.empty_cache()

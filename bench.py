@@ -6,15 +6,20 @@
 One step = one dora_decode_attn call (stream-K decode kernel + combine) over
 one synthetic long-tailed decode batch whose inputs are already resident in
 HBM.  Caches (256 MB Infinity Cache, 8 x 4 MB L2) are evicted by a 1 GiB read
-before every step, outside the timed events.  The main line is the
-7B-class rollout batch (64 sequences, lognormal lengths with median 2048);
-the other workloads and the pack/unpack copy are reported under "workloads".
+before every step, outside the timed events.  The main line is the largest
+batch, the MoE-scale one (1024 sequences, fp8 E4M3 KV with per-page scales,
+32-token pages, lognormal lengths with median 4096); the other workloads and
+the pack/unpack copy are reported under "workloads", each with its own
+roofline object.
 
 Prints one JSON line.  value = decode tokens/s = sequences / step time (every
 sequence advances one token per step).  roofline: the decode kernel's
 algorithmic bytes (K and V of valid tokens, page scales, Q, output, block
 table and lengths) over its average duration, measured with HIP events that
-the library records around each kernel on the launch stream.
+the library records around each kernel on the launch stream
+(dora_decode_attn_timed).  The achievable-bandwidth reference beside the
+8 TB/s peak is the library's own streaming-read kernel (dora_stream_read:
+random 4 KiB tiles, non-temporal loads, the decode kernel's access pattern).
 """
 from __future__ import annotations
 
@@ -34,7 +39,7 @@ import workloads as wl  # noqa: E402
 
 METRIC = "decode-attn tokens/s and HBM GB/s (% of peak) on long-tail length mixes"
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
-MAIN_WORKLOAD = "rollout7b"
+MAIN_WORKLOAD = "moe_fp8"
 PROFILES = os.path.join(ROOT, "profiles")
 DECODE_KERNEL = "dora::decode_kernel"
 CALIBRATION_KERNEL = "__amd_rocclr_copyBuffer"   # the 2 GiB device copy in copy_bandwidth()
@@ -288,7 +293,7 @@ def time_decode(torch, dora, b, steps, warmup, flush, num_waves=0):
 
     def call(prof=None):
         dora.dora_decode_attn(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens,
-                              b.version_ids, out, prof_events=prof, **kw)
+                              b.version_ids, out, events=prof, **kw)
 
     for _ in range(warmup):
         flush()
@@ -450,34 +455,66 @@ def time_offload(torch, dora, b, src_t, dst_t, packed, geo, n_seqs, moved, steps
 
 
 def copy_bandwidth(torch, nbytes=2 << 30):
-    """Measured reference rates: a device copy (read + write) and a read-only
-    reduction, both over 2 GiB."""
+    """A 2 GiB device-to-device copy (the runtime's copy kernel): the rate is
+    context, and its dispatches calibrate the FETCH_SIZE / WRITE_SIZE counters
+    (it reads and writes exactly 2 GiB)."""
     a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1)
     c = torch.empty_like(a)
-    r = torch.empty((), dtype=torch.float32, device="cuda")
-    out = {}
-    for name, fn, moved in (("copy_gbps_measured", lambda: c.copy_(a), 2 * nbytes),
-                            ("read_gbps_measured", lambda: torch.sum(a, dim=0, out=r), nbytes)):
-        for _ in range(3):
-            fn()
-        s, e = make_events(torch, 2)
-        s.record()
-        for _ in range(10):
-            fn()
-        e.record()
-        torch.cuda.synchronize()
-        out[name] = moved / (s.elapsed_time(e) / 10 * 1e-3) / 1e9
+    for _ in range(3):
+        c.copy_(a)
+    s, e = make_events(torch, 2)
+    s.record()
+    for _ in range(10):
+        c.copy_(a)
+    e.record()
+    torch.cuda.synchronize()
+    rate = 2 * nbytes / (s.elapsed_time(e) / 10 * 1e-3) / 1e9
     del a, c
+    return rate
+
+
+def stream_read_reference(torch, dora, flush, steps=10, buf_bytes=8 << 30, read_bytes=1 << 30,
+                          tile=4096):
+    """Achievable read bandwidth with the decode kernel's access pattern: the
+    library's streaming-read kernel (dora_stream_read) over 1 GiB of 4 KiB
+    tiles of an 8 GiB buffer, random or in order, with one wavefront per
+    resident decode slot (5 per CU, as for bf16 pages, and 8 per CU, as for
+    fp8 pages).  Median of `steps` calls, caches evicted before each."""
+    props = torch.cuda.get_device_properties(0)
+    cus = props.multi_processor_count
+    buf = torch.empty(buf_bytes, dtype=torch.uint8, device="cuda")
+    n_all = buf_bytes // tile
+    n = read_bytes // tile
+    rng = np.random.default_rng(4096)
+    orders = {"random": rng.permutation(n_all)[:n].astype(np.int32),
+              "sequential": np.arange(n, dtype=np.int32)}
+    out = {"tile_bytes": tile, "read_bytes": n * tile, "buffer_bytes": buf_bytes}
+    for name, ids in orders.items():
+        tiles = torch.from_numpy(ids).cuda()
+        for per_cu in (5, 8):
+            sink = torch.zeros(cus * per_cu, dtype=torch.int32, device="cuda")
+            ts = time_calls(torch, lambda: dora.dora_stream_read(buf, tiles, sink,
+                                                                 tile_bytes=tile),
+                            steps, 2, flush)
+            ms = float(np.median(ts))
+            out[f"{name}_{per_cu}_per_cu_gbps"] = n * tile / (ms * 1e-3) / 1e9
+        del tiles
+    out["achievable_gbps"] = max(v for k, v in out.items() if k.startswith("random_"))
+    del buf
+    torch.cuda.empty_cache()
     return out
 
 
 def cpu_baseline(b, budget_s=20.0, min_s=10.0):
     """The fp64 oracle on the host cores over the same batch (or a prefix of
     its sequences that fits the time budget), repeated until min_s of work is
-    timed, scaled to decode tokens/s."""
+    timed, scaled to decode tokens/s.  Threads: OMP_NUM_THREADS when set (the
+    host's CPU share for this GPU), else every core in the affinity mask."""
     import oracle
 
-    cores = min(16, len(os.sched_getaffinity(0)))
+    mask = len(os.sched_getaffinity(0))
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    cores = min(mask, int(env)) if env.isdigit() and int(env) > 0 else mask
     order = list(range(b.w.num_seqs))
     # calibrate on one sequence, then take as many sequences as the budget allows
     probe = wl.subset_for_oracle(b, order[:1])
@@ -513,6 +550,8 @@ def cpu_baseline(b, budget_s=20.0, min_s=10.0):
             "sample": f"{len(take)} of {b.w.num_seqs} sequences ({ctx} context tokens), "
                       f"run {reps} times ({total:.1f} s, {dt:.3f} s each), scaled by "
                       f"total/sampled context tokens",
+            "affinity_mask_cores": mask,
+            "threads_source": "OMP_NUM_THREADS" if cores != mask or env else "affinity mask",
             "cpu_model": _cpu_model()}
 
 
@@ -538,6 +577,29 @@ def load_pmc(w):
     if pmc.get("kernel_source_hash") != kernel_source_hash() or pmc.get("workload") != w.name:
         return None
     return pmc
+
+
+def roofline_of(rec, achievable_gbps):
+    """Roofline object of one workload's decode kernel: algorithmic bytes per
+    launch over the kernel's average duration by events; traffic from the
+    committed counter summary when it matches the kernel sources."""
+    ab = rec["algorithmic_bytes"]["total"]
+    ms = rec["split_kernel_ms"]
+    gbps = ab / (ms * 1e-3) / 1e9
+    return {
+        "bound": "hbm",
+        "kernel": "decode_kernel",
+        "achieved": gbps,
+        "peak": HBM_PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": gbps / HBM_PEAK_GBPS,
+        "traffic": rec["split_kernel_traffic_bytes"],
+        "l2_hit_rate": rec["split_kernel_l2_hit_rate"],
+        "algorithmic_bytes_per_launch": ab,
+        "avg_launch_ms": ms,
+        "achievable_gbps": achievable_gbps,
+        "frac_of_achievable": gbps / achievable_gbps,
+    }
 
 
 def main():
@@ -581,7 +643,7 @@ def main():
         return
     names = [args.workload] + ([] if args.only_main else
                                [w.name for w in wl.WORKLOADS if w.name != args.workload])
-    results, main_rec, main_t, main_batch = {}, None, None, None
+    results, main_rec, main_w = {}, None, None
     cpu = None
     for name in names:
         w = wl.BY_NAME[name]
@@ -606,13 +668,12 @@ def main():
         log(f"workload {name}: {rec['ms_per_step']:.4f} ms/step, "
             f"{rec['hbm_gbps']:.0f} GB/s, split kernel {rec['split_kernel_gbps']:.0f} GB/s")
         if name == args.workload:
-            main_rec, main_t, main_batch = rec, t, b
+            main_rec, main_w = rec, w
             main_rec["steps_wall_s"] = t["wall_s"]
             if not args.no_cpu_baseline:
                 log("cpu baseline (oracle)")
                 cpu = cpu_baseline(b)
-        else:
-            del b
+        del b, t
         torch.cuda.empty_cache()
 
     grpo = None
@@ -622,11 +683,12 @@ def main():
         log(f"workload grpo7b: {grpo['plain']['ms_per_step']:.4f} ms/step plain, "
             f"{grpo['grouped']['ms_per_step']:.4f} grouped ({grpo['speedup']:.2f}x)")
         torch.cuda.empty_cache()
-    ref_rates = copy_bandwidth(torch)
-    w = main_batch.w
-    ab = main_rec["algorithmic_bytes"]["total"]
-    split_s = main_rec["split_kernel_ms"] * 1e-3
-    traffic = main_rec["split_kernel_traffic_bytes"]
+    log("streaming-read reference")
+    reference = stream_read_reference(torch, dora, flush)
+    for rec in results.values():
+        rec["roofline"] = roofline_of(rec, reference["achievable_gbps"])
+    copy_gbps = copy_bandwidth(torch)
+    w = main_w
     line = {
         "metric": METRIC,
         "value": main_rec["decode_tokens_per_s"],
@@ -652,19 +714,9 @@ def main():
         "hbm_gbps": main_rec["hbm_gbps"],
         "hbm_frac_of_peak": main_rec["hbm_frac_of_peak"],
         "context_tokens_per_s": main_rec["context_tokens_per_s"],
-        **ref_rates,
-        "roofline": {
-            "bound": "hbm",
-            "kernel": "decode_kernel",
-            "achieved": ab / split_s / 1e9,
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": ab / split_s / 1e9 / HBM_PEAK_GBPS,
-            "traffic": traffic,
-            "l2_hit_rate": main_rec["split_kernel_l2_hit_rate"],
-            "algorithmic_bytes_per_launch": ab,
-            "avg_launch_ms": main_rec["split_kernel_ms"],
-        },
+        "roofline": main_rec["roofline"],
+        "stream_read_reference": reference,
+        "copy_gbps_measured": copy_gbps,
         "cpu_baseline": cpu,
         "flush_between_steps": None if args.no_flush else args.flush_mode,
         "timing_event_flags": hex(EVENT_FLAGS),

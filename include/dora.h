@@ -171,6 +171,31 @@ dora_status dora_decode_attn(const dora_decode_desc* desc,
                              void* workspace, size_t workspace_bytes,
                              dora_stream_t stream);
 
+/* Size of the fixed device array dora_decode_attn_noalloc uses as its
+ * workspace, one per GPU. */
+#define DORA_NOALLOC_WORKSPACE_BYTES ((size_t)48 << 20)
+
+/* dora_decode_attn for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * Same arguments, results and errors as dora_decode_attn, without the
+ * workspace: the call uses a fixed array of DORA_NOALLOC_WORKSPACE_BYTES in
+ * device memory that the library holds on each GPU it runs on, from load until
+ * the process ends.  It allocates and frees nothing; its first call on a device
+ * looks the array's address up.
+ *   DORA_ERR_WORKSPACE_TOO_SMALL  dora_decode_workspace_bytes(desc) exceeds the
+ *                                 array (e.g. a large desc->num_waves)
+ *   DORA_ERR_INVALID_ARG          DORA_FLAG_VALIDATE set (it synchronises and
+ *                                 copies to the host); plus dora_decode_attn's
+ * Every call on one GPU uses that GPU's array, and the array keeps the last
+ * call's contents (the decode ignores them): calls that overlap on one GPU (on
+ * different streams or from different threads) race, and the caller must
+ * order them. */
+dora_status dora_decode_attn_noalloc(const dora_decode_desc* desc,
+                                     const void* q, const void* k_pages, const void* v_pages,
+                                     const int32_t* block_table, const int32_t* seq_lens,
+                                     const int32_t* version_ids, void* out,
+                                     dora_stream_t stream);
+
 /* Decode attention for a batch made of response groups that share a prompt
  * (the responses sampled per prompt for GRPO-style advantages, App. B).  The
  * result equals dora_decode_attn's on the same arguments (up to fp32 rounding);

@@ -22,7 +22,8 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdora.so")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["decode.hip", "pack.hip", "append.hip", "grouped.hip", "measure.hip"]
+HIP_SOURCES = ["decode.hip", "pack.hip", "append.hip", "grouped.hip", "measure.hip",
+               "noalloc.hip"]
 CXX_SOURCES = ["api.cpp", "pool.cpp", "plan.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}"]

@@ -81,6 +81,8 @@ _lib.dora_stream_read.argtypes = [_P, _I64, _P, _I64, _I32, _P, _I32, _P]
 _lib.dora_stream_read.restype = ctypes.c_int
 _lib.dora_decode_attn.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
 _lib.dora_decode_attn.restype = ctypes.c_int
+_lib.dora_decode_attn_noalloc.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P]
+_lib.dora_decode_attn_noalloc.restype = ctypes.c_int
 _lib.dora_decode_grouped_workspace_bytes.argtypes = [_DescP, _I32]
 _lib.dora_decode_grouped_workspace_bytes.restype = _SZ
 _lib.dora_decode_attn_grouped.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _I32, _P, _P,
@@ -335,6 +337,29 @@ def dora_decode_attn(q, k_pages, v_pages, block_table, seq_lens, version_ids, ou
         st = _lib.dora_decode_attn_timed(ctypes.byref(desc), *args, ws_ptr, workspace.numel(),
                                          _stream_handle(stream), ctypes.cast(arr, _P))
         _check(st, "dora_decode_attn_timed")
+    return out
+
+
+NOALLOC_WORKSPACE_BYTES = 48 << 20   # DORA_NOALLOC_WORKSPACE_BYTES
+
+
+def dora_decode_attn_noalloc(q, k_pages, v_pages, block_table, seq_lens, version_ids, out, *,
+                             num_kv_heads: int, page_size: int, kv_dtype: int = DORA_KV_BF16,
+                             sm_scale: float = 0.0, k_scales=None, v_scales=None,
+                             page_owner=None, flags: int = 0, num_waves: int = 0,
+                             min_range_pages: int = 0, stream=None):
+    """dora_decode_attn with the library's fixed per-GPU workspace: neither the
+    library nor this wrapper allocates device memory.  Calls that overlap on
+    one GPU race on that workspace (see include/dora.h).  Returns `out`."""
+    desc, args = _decode_args(q, k_pages, v_pages, block_table, seq_lens, version_ids, out,
+                              num_kv_heads=num_kv_heads, page_size=page_size,
+                              kv_dtype=kv_dtype, sm_scale=sm_scale, k_scales=k_scales,
+                              v_scales=v_scales, page_owner=page_owner, flags=flags,
+                              num_waves=num_waves, min_range_pages=min_range_pages)
+    if args is None:
+        return out
+    _check(_lib.dora_decode_attn_noalloc(ctypes.byref(desc), *args, _stream_handle(stream)),
+           "dora_decode_attn_noalloc")
     return out
 
 

@@ -285,3 +285,26 @@ def test_measure_entry_points_reject_bad_arguments(d):
     assert sr(P(FAKE), 1 << 20, None, 4, 4096, P(FAKE), 8, None) == d.DORA_ERR_INVALID_ARG
     assert sr(P(FAKE), 1 << 20, P(FAKE), -1, 4096, P(FAKE), 8, None) == d.DORA_ERR_INVALID_ARG
     assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 3072, P(FAKE), 8, None) == d.DORA_ERR_UNSUPPORTED
+
+
+def test_noalloc_entry_refuses_before_any_launch(d):
+    """dora_decode_attn_noalloc: a workspace beyond its fixed array, the
+    VALIDATE flag and invalid descriptors are refused on the host."""
+    P = ctypes.c_void_p
+    lib = d.library()
+    args = [P(FAKE)] * 7 + [None]
+    big = _desc(d, num_waves=200000)
+    assert d.dora_decode_workspace_bytes(big) > d.NOALLOC_WORKSPACE_BYTES
+    assert lib.dora_decode_attn_noalloc(ctypes.byref(big), *args) == \
+        d.DORA_ERR_WORKSPACE_TOO_SMALL
+    val = _desc(d, flags=d.DORA_FLAG_VALIDATE)
+    assert lib.dora_decode_attn_noalloc(ctypes.byref(val), *args) == d.DORA_ERR_INVALID_ARG
+    bad = _desc(d, head_dim=96)
+    assert lib.dora_decode_attn_noalloc(ctypes.byref(bad), *args) == d.DORA_ERR_UNSUPPORTED
+    assert lib.dora_decode_attn_noalloc(None, *args) == d.DORA_ERR_INVALID_ARG
+    # every supported geometry fits at the default launch of a 256-CU part
+    for hd in (64, 128):
+        for dt in (0, 1):
+            full = _desc(d, num_seqs=8192, num_q_heads=128, num_kv_heads=8, head_dim=hd,
+                         kv_dtype=dt, block_table_stride=4096)
+            assert 0 < d.dora_decode_workspace_bytes(full) <= d.NOALLOC_WORKSPACE_BYTES

@@ -54,6 +54,18 @@ PMC_CMD = ("cd /tmp && timeout -s KILL 300 rocprofv3 --pmc {c} --output-format c
            "-d $REPO/gpurun_out/pmc_{d}_{w} -o run -- python $REPO/bench.py --only-main "
            "--workload {w} --no-cpu-baseline --steps 5 --warmup 1")
 L2_COUNTERS = "TCC_HIT_sum TCC_MISS_sum"
+# Compute-side counters, three rocprofv3 --pmc passes (at most 8 SQ counters
+# and 2 GRBM counters per pass; VmemLatency and MemUnitStalled are rocprofv3's
+# derived metrics).
+COMPUTE_PASSES = {
+    "C1": ("SQ_INSTS_VALU SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES SQ_WAVES "
+           "SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_INSTS_VALU_CVT GRBM_GUI_ACTIVE"),
+    "C2": ("SQ_ACTIVE_INST_VALU SQ_INSTS_VMEM_RD SQ_INSTS_SALU SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT "
+           "SQ_ACTIVE_INST_ANY SQ_WAIT_ANY SQ_BUSY_CYCLES GRBM_GUI_ACTIVE"),
+    "C3": "VmemLatency MemUnitStalled",
+}
+COMPUTE_CMD = ("cd /tmp && timeout -s KILL 300 rocprofv3 --pmc {c} --output-format csv "
+               "-d $REPO/gpurun_out/pmc_{p}_{w} -o run -- python $REPO/bench.py {args}")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2604_26256_amd", "csrc", f)
                   for f in ("decode.hip", "decode_core.h", "dora_internal.h", "api.cpp")]
 
@@ -94,6 +106,9 @@ def parse():
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "L2_DIR"),
                     help="write the HBM-traffic and L2 hit-rate summary of three "
                          "rocprofv3 --pmc runs")
+    ap.add_argument("--summarize-compute", nargs=4, metavar=("WORKLOAD", "C1", "C2", "C3"),
+                    help="write the compute-side counter summary of three rocprofv3 --pmc "
+                         "runs (WORKLOAD: a workload name or grpo7b)")
     return ap.parse_args()
 
 
@@ -209,6 +224,107 @@ def summarize_pmc(fetch_dir, write_dir, l2_dir, workload):
     out = pmc_path(workload)
     json.dump(summary, open(out, "w"), indent=1)
     print(out)
+
+
+def compute_bench_args(workload):
+    return ("--grpo-only --steps 5" if workload == "grpo7b" else
+            f"--only-main --workload {workload} --no-cpu-baseline --steps 5 --warmup 1")
+
+
+def compute_path(workload):
+    return os.path.join(PROFILES, f"compute_counters_{workload}.json")
+
+
+def _work_units(workload):
+    """Work per launch of the decode-attention kernels of a bench run, in
+    (page, KV head) steps of 16 query columns: {kernel name fragment: units}."""
+    if workload == "grpo7b":
+        w, M = wl.GRPO_WORKLOAD, wl.GRPO_GROUP
+        lengths, shared = wl.grpo_lengths()
+        n = wl.pages_needed(lengths, w.page_size)
+        tiles = -(-(M * w.group) // 16)            # column tiles of a group's prefix
+        lead = shared[::M].astype(np.int64)
+        return {"decode_kernel<128, 16, false, 3, false>": int(n.sum()) * w.num_kv_heads,
+                "decode_kernel<128, 16, false, 3, true>": int((n - shared).sum()) *
+                w.num_kv_heads,
+                "prefix_kernel": int(lead.sum()) * w.num_kv_heads * tiles}
+    w = wl.BY_NAME[workload]
+    lengths = wl.sample_lengths(w, wl.seeds(wl.WORKLOADS.index(w))[0])
+    return {"decode_kernel": int(wl.pages_needed(lengths, w.page_size).sum()) * w.num_kv_heads}
+
+
+def summarize_compute(dirs, workload):
+    """Per-dispatch averages of the compute-side counters of every library
+    kernel in three --pmc runs, with derived figures: MFMA and VALU busy
+    fractions of the SIMDs, the share of wave time spent waiting, mean
+    resident waves per CU, the engine clock over the dispatch, and, for the
+    decode-attention kernels, instructions per (page, KV head, 16-column)
+    step."""
+    import csv
+
+    agent = None
+    per = {}
+    for d in dirs:
+        for r in csv.DictReader(open(_find_csv(d, "agent_info.csv"))):
+            if r["Agent_Type"] == "GPU":
+                agent = r
+        for r in csv.DictReader(open(_find_csv(d, "counter_collection.csv"))):
+            k = r["Kernel_Name"]
+            if not k.startswith(("dora::", "void dora::")):
+                continue
+            e = per.setdefault(k, {"counters": {}, "durations_ns": []})
+            e["counters"].setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+            if r["Counter_Name"] == "GRBM_GUI_ACTIVE" and d == dirs[0]:
+                e["durations_ns"].append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    xcc, cus, simds = int(agent["Num_Xcc"]), int(agent["Cu_Count"]), int(agent["Simd_Count"])
+    units = _work_units(workload)
+    kernels = {}
+    for k, e in per.items():
+        c = {n: sum(v) / len(v) for n, v in e["counters"].items()}
+        dur = sum(e["durations_ns"]) / max(1, len(e["durations_ns"]))
+        gui = c.get("GRBM_GUI_ACTIVE", 0.0) / xcc          # cycles of one XCC
+        der = {}
+        if gui > 0:
+            der["engine_clock_ghz"] = gui / dur if dur else None
+            der["mfma_busy_frac"] = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (gui * simds)
+            der["valu_busy_frac"] = 4 * c.get("SQ_ACTIVE_INST_VALU", 0.0) / (gui * simds)
+            der["mean_waves_per_cu"] = 4 * c.get("SQ_WAVE_CYCLES", 0.0) / (gui * cus)
+            der["lds_bank_conflict_frac_of_cu_time"] = \
+                c.get("SQ_LDS_BANK_CONFLICT", 0.0) / (gui * cus)
+        if c.get("SQ_WAVE_CYCLES"):
+            der["wave_wait_any_frac"] = c.get("SQ_WAIT_ANY", 0.0) / c["SQ_WAVE_CYCLES"]
+            der["wave_wait_inst_frac"] = c.get("SQ_WAIT_INST_ANY", 0.0) / c["SQ_WAVE_CYCLES"]
+        der["vmem_latency_cycles"] = c.get("VmemLatency")
+        u = next((v for frag, v in units.items() if frag in k), None)
+        if u:
+            der["steps_per_launch"] = u
+            for n in ("SQ_INSTS_MFMA", "SQ_INSTS_VALU", "SQ_INSTS_VALU_CVT", "SQ_INSTS_SALU",
+                      "SQ_INSTS_VMEM_RD", "SQ_INSTS_LDS"):
+                if n in c:
+                    der[n.lower().replace("sq_insts_", "") + "_per_step"] = c[n] / u
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in c:
+                der["mfma_busy_cycles_per_step"] = c["SQ_VALU_MFMA_BUSY_CYCLES"] / u
+        kernels[k] = {"dispatches": len(e["durations_ns"]), "avg_duration_us": dur / 1e3,
+                      "counters_per_dispatch": c, "derived": der}
+    out = {
+        "workload": workload,
+        "kernel_source_hash": kernel_source_hash(),
+        "commands": [COMPUTE_CMD.format(c=f'"{v}"', p=p, w=workload,
+                                        args=compute_bench_args(workload))
+                     for p, v in COMPUTE_PASSES.items()],
+        "device": {"cus": cus, "simds": simds, "xcc": xcc,
+                   "max_engine_clock_mhz": int(agent["Max_Engine_Clk_Fcompute"])},
+        "notes": ["Counters are summed over all XCCs, shader engines and SIMDs by rocprofv3;",
+                  "GRBM_GUI_ACTIVE / xcc is the dispatch's length in engine cycles.",
+                  "SQ_ACTIVE_INST_VALU, SQ_WAVE_CYCLES, SQ_WAIT_ANY and SQ_WAIT_INST_ANY are",
+                  "quad-cycle counts (x4 to cycles); SQ_VALU_MFMA_BUSY_CYCLES is in cycles.",
+                  "A step is one (page, KV head) for 16 query columns (a prefix step covers",
+                  "one column tile of a group's shared page)."],
+        "kernels": kernels,
+    }
+    os.makedirs(PROFILES, exist_ok=True)
+    json.dump(out, open(compute_path(workload), "w"), indent=1)
+    print(compute_path(workload))
 
 
 # Timing events.  HIP events made with hipEventDisableSystemFence skip the
@@ -477,9 +593,12 @@ def stream_read_reference(torch, dora, flush, steps=10, buf_bytes=8 << 30, read_
                           tile=4096):
     """Achievable read bandwidth with the decode kernel's access pattern: the
     library's streaming-read kernel (dora_stream_read) over 1 GiB of 4 KiB
-    tiles of an 8 GiB buffer, random or in order, with one wavefront per
-    resident decode slot (5 per CU, as for bf16 pages, and 8 per CU, as for
-    fp8 pages).  Median of `steps` calls, caches evicted before each."""
+    tiles of an 8 GiB buffer, in random or in sequential order, swept over
+    the wavefronts per CU (5, as the decode launches for bf16 pages, and 8,
+    every resident slot, as for fp8 pages) and the tiles each wavefront keeps
+    per batch (1, 2 or 4, two batches in flight).  Median of `steps` calls per
+    variant, caches evicted before each; achievable_gbps is the best random
+    variant."""
     props = torch.cuda.get_device_properties(0)
     cus = props.multi_processor_count
     buf = torch.empty(buf_bytes, dtype=torch.uint8, device="cuda")
@@ -488,18 +607,20 @@ def stream_read_reference(torch, dora, flush, steps=10, buf_bytes=8 << 30, read_
     rng = np.random.default_rng(4096)
     orders = {"random": rng.permutation(n_all)[:n].astype(np.int32),
               "sequential": np.arange(n, dtype=np.int32)}
-    out = {"tile_bytes": tile, "read_bytes": n * tile, "buffer_bytes": buf_bytes}
+    out = {"tile_bytes": tile, "read_bytes": n * tile, "buffer_bytes": buf_bytes,
+           "gbps": {}}
     for name, ids in orders.items():
         tiles = torch.from_numpy(ids).cuda()
         for per_cu in (5, 8):
             sink = torch.zeros(cus * per_cu, dtype=torch.int32, device="cuda")
-            ts = time_calls(torch, lambda: dora.dora_stream_read(buf, tiles, sink,
-                                                                 tile_bytes=tile),
-                            steps, 2, flush)
-            ms = float(np.median(ts))
-            out[f"{name}_{per_cu}_per_cu_gbps"] = n * tile / (ms * 1e-3) / 1e9
+            for tpb in (1, 2, 4):
+                ts = time_calls(torch, lambda: dora.dora_stream_read(
+                    buf, tiles, sink, tile_bytes=tile, tiles_per_batch=tpb), steps, 2, flush)
+                ms = float(np.median(ts))
+                out["gbps"][f"{name}_{per_cu}_per_cu_{tpb}_tiles"] = n * tile / (ms * 1e-3) / 1e9
         del tiles
-    out["achievable_gbps"] = max(v for k, v in out.items() if k.startswith("random_"))
+    best = max((v, k) for k, v in out["gbps"].items() if k.startswith("random_"))
+    out["achievable_gbps"], out["achievable_variant"] = best
     del buf
     torch.cuda.empty_cache()
     return out
@@ -606,6 +727,9 @@ def main():
     global EVENT_FLAGS
     args = parse()
     EVENT_FLAGS = args.event_flags
+    if args.summarize_compute:
+        summarize_compute(args.summarize_compute[1:], args.summarize_compute[0])
+        return
     if args.summarize_trace or args.summarize_pmc or args.summarize_grpo_trace:
         if args.summarize_grpo_trace:
             summarize_trace(args.summarize_grpo_trace, None, grpo=True)

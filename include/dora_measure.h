@@ -34,19 +34,23 @@ dora_status dora_decode_attn_timed(const dora_decode_desc* desc,
 /* Streaming-read reference kernel.  Reads n_tiles tiles of tile_bytes bytes,
  * tile i starting at base + tiles[i] * tile_bytes, with 16-byte non-temporal
  * loads.  `waves` one-wavefront workgroups each take an equal contiguous range
- * of the tile list (the first n_tiles mod waves ranges one tile more), keep
- * several tiles in flight, and fold every byte they read into one 32-bit word,
- * written to sink[w] (so that no load is dead).
+ * of the tile list (the first n_tiles mod waves ranges one tile more), read it
+ * in batches of tiles_per_batch tiles with two batches in flight, and fold
+ * every word they read into one 32-bit XOR, written to sink[w] (so that no
+ * load is dead).
  *   base        device, 16-byte aligned, base_bytes bytes
  *   tiles       device int32 [n_tiles]; a tile that does not lie inside
- *               [base, base + base_bytes) is skipped (not read)
- *   tile_bytes  1024, 2048, 4096, 8192 or 16384 (else DORA_ERR_UNSUPPORTED)
+ *               [base, base + base_bytes) contributes nothing (its loads go to
+ *               the buffer's first 16 bytes)
+ *   tile_bytes  1024, 2048, 4096, 8192 or 16384
+ *   tiles_per_batch  1, 2, 4, 8 or 16, with tile_bytes * tiles_per_batch at
+ *               most 16384 (else, like another tile_bytes, DORA_ERR_UNSUPPORTED)
  *   sink        device uint32 [waves]
  *   waves       >= 1
  * n_tiles = 0 writes 0 to every sink word. */
 dora_status dora_stream_read(const void* base, int64_t base_bytes, const int32_t* tiles,
-                             int64_t n_tiles, int32_t tile_bytes, uint32_t* sink,
-                             int32_t waves, dora_stream_t stream);
+                             int64_t n_tiles, int32_t tile_bytes, int32_t tiles_per_batch,
+                             uint32_t* sink, int32_t waves, dora_stream_t stream);
 
 #ifdef __cplusplus
 }

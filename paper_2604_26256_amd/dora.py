@@ -77,7 +77,7 @@ _lib.dora_decode_num_waves.argtypes = [_DescP]
 _lib.dora_decode_num_waves.restype = _I64
 _lib.dora_decode_attn_timed.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P]
 _lib.dora_decode_attn_timed.restype = ctypes.c_int
-_lib.dora_stream_read.argtypes = [_P, _I64, _P, _I64, _I32, _P, _I32, _P]
+_lib.dora_stream_read.argtypes = [_P, _I64, _P, _I64, _I32, _I32, _P, _I32, _P]
 _lib.dora_stream_read.restype = ctypes.c_int
 _lib.dora_decode_attn.argtypes = [_DescP, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
 _lib.dora_decode_attn.restype = ctypes.c_int
@@ -363,16 +363,18 @@ def dora_decode_attn_noalloc(q, k_pages, v_pages, block_table, seq_lens, version
     return out
 
 
-def dora_stream_read(base, tiles, sink, *, tile_bytes=4096, stream=None):
+def dora_stream_read(base, tiles, sink, *, tile_bytes=4096, tiles_per_batch=4, stream=None):
     """Streaming-read reference (include/dora_measure.h): read the tiles of
     `base` (device uint8) listed in `tiles` (device int32) with non-temporal
-    loads, one wavefront per entry of `sink` (device int32/uint32 words)."""
+    loads, tiles_per_batch tiles per batch and two batches in flight, one
+    wavefront per entry of `sink` (device int32/uint32 words)."""
     torch = _torch()
     n = int(tiles.numel())
     st = _lib.dora_stream_read(
         _dev_ptr(base, "base", (torch.uint8,)), base.numel(),
         _dev_ptr(tiles, "tiles", (torch.int32,), numel=n, align=4) if n else None, n,
-        int(tile_bytes), _dev_ptr(sink, "sink", (torch.int32, torch.uint32), align=4),
+        int(tile_bytes), int(tiles_per_batch),
+        _dev_ptr(sink, "sink", (torch.int32, torch.uint32), align=4),
         int(sink.numel()), _stream_handle(stream))
     _check(st, "dora_stream_read")
     return sink

@@ -277,14 +277,17 @@ def test_measure_entry_points_reject_bad_arguments(d):
     assert lib.dora_decode_attn_timed(ctypes.byref(bad), *args,
                                       ctypes.cast(ev_ok, P)) == d.DORA_ERR_UNSUPPORTED
     sr = lib.dora_stream_read
-    assert sr(None, 1 << 20, P(FAKE), 4, 4096, P(FAKE), 8, None) == d.DORA_ERR_INVALID_ARG
-    assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 4096, None, 8, None) == d.DORA_ERR_INVALID_ARG
-    assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 4096, P(FAKE), 0, None) == d.DORA_ERR_INVALID_ARG
-    assert sr(P(FAKE + 4), 1 << 20, P(FAKE), 4, 4096, P(FAKE), 8, None) == \
+    assert sr(None, 1 << 20, P(FAKE), 4, 4096, 4, P(FAKE), 8, None) == d.DORA_ERR_INVALID_ARG
+    assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 4096, 4, None, 8, None) == d.DORA_ERR_INVALID_ARG
+    assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 4096, 4, P(FAKE), 0, None) == d.DORA_ERR_INVALID_ARG
+    assert sr(P(FAKE + 4), 1 << 20, P(FAKE), 4, 4096, 4, P(FAKE), 8, None) == \
         d.DORA_ERR_INVALID_ARG
-    assert sr(P(FAKE), 1 << 20, None, 4, 4096, P(FAKE), 8, None) == d.DORA_ERR_INVALID_ARG
-    assert sr(P(FAKE), 1 << 20, P(FAKE), -1, 4096, P(FAKE), 8, None) == d.DORA_ERR_INVALID_ARG
-    assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 3072, P(FAKE), 8, None) == d.DORA_ERR_UNSUPPORTED
+    assert sr(P(FAKE), 1 << 20, None, 4, 4096, 4, P(FAKE), 8, None) == d.DORA_ERR_INVALID_ARG
+    assert sr(P(FAKE), 1 << 20, P(FAKE), -1, 4096, 4, P(FAKE), 8, None) == \
+        d.DORA_ERR_INVALID_ARG
+    assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 3072, 4, P(FAKE), 8, None) == d.DORA_ERR_UNSUPPORTED
+    assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 4096, 8, P(FAKE), 8, None) == d.DORA_ERR_UNSUPPORTED
+    assert sr(P(FAKE), 1 << 20, P(FAKE), 4, 4096, 3, P(FAKE), 8, None) == d.DORA_ERR_UNSUPPORTED
 
 
 def test_noalloc_entry_refuses_before_any_launch(d):

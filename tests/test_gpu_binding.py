@@ -71,9 +71,9 @@ def test_two_streams_do_not_share_a_workspace(grouped):
             assert torch.equal(o.view(torch.int16), r.view(torch.int16)), rep
 
 
-@pytest.mark.parametrize("tile", [1024, 4096, 16384])
-def test_stream_read_checksums(tile):
-    print(f"[case] stream read tile={tile}", flush=True)
+@pytest.mark.parametrize("tile,tpb", [(1024, 16), (1024, 1), (4096, 1), (4096, 4), (16384, 1)])
+def test_stream_read_checksums(tile, tpb):
+    print(f"[case] stream read tile={tile} tiles per batch={tpb}", flush=True)
     d = lib()
     nbytes = 32 << 20
     g = torch.Generator(device="cuda").manual_seed(tile)
@@ -85,7 +85,8 @@ def test_stream_read_checksums(tile):
     ids[100] = -2           # negative: skipped
     waves = 37
     sink = torch.full((waves,), 0x5A5A, dtype=torch.int32, device="cuda")
-    d.dora_stream_read(buf, torch.from_numpy(ids).cuda(), sink, tile_bytes=tile)
+    d.dora_stream_read(buf, torch.from_numpy(ids).cuda(), sink, tile_bytes=tile,
+                       tiles_per_batch=tpb)
     torch.cuda.synchronize()
     words = buf.cpu().numpy().view(np.uint32).reshape(n_all, tile // 4)
     q, rem = divmod(len(ids), waves)

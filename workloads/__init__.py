@@ -345,6 +345,21 @@ GRPO_GROUP = 16
 GRPO_PROMPT = (1024, 4096)
 
 
+def grpo_lengths(w: Workload = GRPO_WORKLOAD, group_size: int = GRPO_GROUP,
+                 prompt_range=GRPO_PROMPT, seed_index: int = 5):
+    """Lengths of a GRPO-shaped batch (prompt plus response per member) and
+    each member's shared full prompt pages: (lengths int32 [B], shared int32
+    [B])."""
+    sd = seeds(seed_index)
+    rng = np.random.default_rng(sd[6])
+    n_groups = w.num_seqs // group_size
+    assert n_groups * group_size == w.num_seqs
+    prompt = rng.integers(prompt_range[0], prompt_range[1] + 1, n_groups)
+    lengths = (np.repeat(prompt, group_size) + sample_lengths(w, sd[0])).astype(np.int32)
+    shared = np.repeat(prompt // w.page_size, group_size).astype(np.int32)
+    return lengths, shared
+
+
 def make_grpo_batch(w: Workload = GRPO_WORKLOAD, group_size: int = GRPO_GROUP,
                     prompt_range=GRPO_PROMPT, device="cpu", seed_index: int = 5,
                     poison: bool = True):
@@ -354,14 +369,9 @@ def make_grpo_batch(w: Workload = GRPO_WORKLOAD, group_size: int = GRPO_GROUP,
     copy-on-write pool).  Returns (batch, shared_pages int32 [B])."""
     import torch
 
-    sd = seeds(seed_index)
-    rng = np.random.default_rng(sd[6])
+    lengths, shared = grpo_lengths(w, group_size, prompt_range, seed_index)
     n_groups = w.num_seqs // group_size
-    assert n_groups * group_size == w.num_seqs
-    prompt = rng.integers(prompt_range[0], prompt_range[1] + 1, n_groups)
-    lengths = (np.repeat(prompt, group_size) + sample_lengths(w, sd[0])).astype(np.int32)
     b = make_batch(w, device=device, seed_index=seed_index, lengths=lengths, poison=poison)
-    shared = np.repeat(prompt // w.page_size, group_size).astype(np.int32)
     bt = b.block_table_h.copy()
     for g in range(n_groups):
         lead = g * group_size

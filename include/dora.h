@@ -122,8 +122,10 @@ typedef struct {
                                   (page, KV head) units; 0 = library default */
 } dora_decode_desc;
 
-/* Human-readable name of a status code (static storage). */
-const char* dora_status_string(dora_status s);
+/* Human-readable name of a status code (static storage); "unknown status" for
+ * a value that is no dora_status.  The code is passed as an int, so any value
+ * is a valid argument. */
+const char* dora_status_string(int status);
 
 /* Bytes of device workspace dora_decode_attn needs for this geometry on the
  * current device (valid for every seq_lens the call may see).  Returns 0 for an

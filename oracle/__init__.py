@@ -21,7 +21,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "dora_oracle.c")
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# DORA_ORACLE_LIBRARY selects another build of the same source (the
+# sanitizer build of the CPU checks); default: the in-tree one.
+_LIB_PATH = os.environ.get("DORA_ORACLE_LIBRARY") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 ERR_NAMES = {0: "ok", 1: "invalid argument", 2: "page out of range", 3: "version mismatch",

@@ -96,8 +96,8 @@ bool ws_layout(const dora_decode_desc& d, int64_t waves, WsLayout* out) {
 
 extern "C" {
 
-const char* dora_status_string(dora_status s) {
-  switch (s) {
+const char* dora_status_string(int status) {
+  switch (status) {
     case DORA_OK: return "ok";
     case DORA_ERR_INVALID_ARG: return "invalid argument";
     case DORA_ERR_UNSUPPORTED: return "unsupported geometry or dtype";

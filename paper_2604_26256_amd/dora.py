@@ -16,7 +16,9 @@ from typing import Optional, Sequence
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libdora.so")
+# DORA_LIBRARY selects another build of the library (the host-sanitizer build
+# of the CPU checks); default: the in-tree gfx950 build.
+LIB_PATH = os.environ.get("DORA_LIBRARY") or os.path.join(_PKG, "libdora.so")
 
 DORA_OK = 0
 DORA_ERR_INVALID_ARG = 1

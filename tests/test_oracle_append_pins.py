@@ -6,7 +6,10 @@ of whole sequences.  For fp8 pages the oracle also keeps one fp32 scale per
 page under a grow-only policy; its encoder is pinned to torch's float8_e4m3fn
 conversion, and the policy to the cases that reduce to that conversion: the
 first token of a page, tokens that fit the current scale, and a scale that
-grows by an exact power of two.
+grows by an exact power of two.  Growth by any other ratio is pinned by exact
+rational arithmetic in which each fp32 step of the stated policy is rounded
+once, on data chosen (by exhaustive search over the E4M3 codes) so that the
+other association of the requantisation product gives other codes.
 """
 import numpy as np
 import pytest
@@ -255,3 +258,154 @@ def test_append_fp8_token_with_the_page_maximum_does_not_grow_the_scale():
     assert ks[page] == snap[2] and vs[page] == snap[3]
     assert np.array_equal(_k_slot(k, page, 0), _k_slot(snap[0][None], 0, 0))
     assert np.array_equal(k[page], snap[0]) and np.array_equal(v[page], snap[1])
+
+
+# ---------------------------------------------------------------------------
+# fp8: a scale that grows by a ratio that is no power of two, pinned by exact
+# rational arithmetic with each fp32 step of the policy rounded explicitly
+# ---------------------------------------------------------------------------
+
+from fractions import Fraction  # noqa: E402
+
+
+def _bf16_exact(code: int) -> Fraction:
+    """Value of a bf16 code from its fields (sign, 8-bit exponent, 7-bit
+    mantissa); finite codes only."""
+    s, e, m = (code >> 15) & 1, (code >> 7) & 0xFF, code & 0x7F
+    assert e != 0xFF
+    v = Fraction(m, 128) * Fraction(2) ** -126 if e == 0 else \
+        (1 + Fraction(m, 128)) * Fraction(2) ** (e - 127)
+    return -v if s else v
+
+
+def _round_even(q: Fraction) -> int:
+    n = q.numerator // q.denominator
+    r = q - n
+    return n + 1 if r > Fraction(1, 2) or (r == Fraction(1, 2) and n % 2) else n
+
+
+def _fl32(q: Fraction) -> Fraction:
+    """Nearest binary32 value (ties to even), normal or subnormal."""
+    if q == 0:
+        return Fraction(0)
+    a = abs(q)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    while Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    ulp = Fraction(2) ** (max(e, -126) - 23)
+    r = _round_even(a / ulp) * ulp
+    assert r < Fraction(2) ** 128
+    return r if q > 0 else -r
+
+
+def _e4m3_exact(code: int) -> Fraction:
+    s, e, m = (code >> 7) & 1, (code >> 3) & 0xF, code & 7
+    assert not (e == 15 and m == 7)
+    v = Fraction(m, 8) * Fraction(2) ** -6 if e == 0 else \
+        (1 + Fraction(m, 8)) * Fraction(2) ** (e - 7)
+    return -v if s else v
+
+
+def _e4m3_enc(x: Fraction) -> int:
+    """Nearest OCP E4M3FN code, ties to even mantissa, saturating at 448."""
+    sign = 0x80 if x < 0 else 0
+    a = abs(x)
+    if a >= 448:
+        return sign | 0x7E
+    e = -6
+    while e < 8 and Fraction(2) ** (e + 1) <= a:
+        e += 1
+    n = _round_even(a / Fraction(2) ** (e - 3))   # units of the grid step at exponent e
+    if e == -6 and n < 8:                         # subnormal (n = 8 is the smallest normal)
+        return sign | n
+    if n == 16:                                   # rounded up to the next binade
+        e, n = e + 1, 8
+    code = ((e + 7) << 3) | (n - 8)
+    return sign | min(code, 0x7E)
+
+
+def _exact_two_token_page(x0_codes, x1_codes):
+    """The stated policy on a page that receives token 0 then token 1 (both as
+    bf16 codes), every fp32 operation rounded once: returns (codes of token 0
+    after token 1, codes of token 1, final scale)."""
+    x0 = [_bf16_exact(int(c)) for c in x0_codes]
+    x1 = [_bf16_exact(int(c)) for c in x1_codes]
+    fresh = lambda xs: max(_fl32(max(abs(v) for v in xs) / 448), Fraction(2) ** -126)  # noqa
+    s0 = fresh(x0)
+    c0 = [_e4m3_enc(_fl32(v / s0)) for v in x0]
+    f1 = fresh(x1)
+    assert not f1 <= s0                                   # the page grows
+    s = f1
+    re0 = [_e4m3_enc(_fl32(_fl32(_e4m3_exact(c) * s0) / s)) for c in c0]
+    c1 = [_e4m3_enc(_fl32(v / s)) for v in x1]
+    # the association the policy does not use, to check the data tell them apart
+    alt0 = [_e4m3_enc(_fl32(_e4m3_exact(c) * _fl32(s0 / s))) for c in c0]
+    return re0, c1, s, alt0
+
+
+def _bf16_code(q: Fraction) -> int:
+    """Nearest bf16 code (ties to even) of a value in the normal range."""
+    sign = 0x8000 if q < 0 else 0
+    a = abs(q)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    while Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    n = _round_even(a / Fraction(2) ** (e - 7))
+    if n == 256:
+        e, n = e + 1, 128
+    return sign | ((e + 127) << 7) | (n - 128)
+
+
+def _discriminating_token(amax0: Fraction, amax1: Fraction, width: int):
+    """bf16 codes of a token 0 whose maximum is amax0 and whose other values
+    requantise differently under the two associations once a token with
+    maximum amax1 grows the page (found by exhaustive search over the E4M3
+    codes), padded with the first such value."""
+    s0 = max(_fl32(amax0 / 448), Fraction(2) ** -126)
+    s = max(_fl32(amax1 / 448), Fraction(2) ** -126)
+    picks = []
+    for c in range(1, 0x7F):
+        a = _e4m3_enc(_fl32(_fl32(_e4m3_exact(c) * s0) / s))
+        b = _e4m3_enc(_fl32(_e4m3_exact(c) * _fl32(s0 / s)))
+        if a == b:
+            continue
+        x = _bf16_code(_e4m3_exact(c) * s0)      # a bf16 value that encodes to c at s0
+        if _e4m3_enc(_fl32(_bf16_exact(x) / s0)) == c and _bf16_exact(x) < amax0:
+            picks.append(x)
+    codes = [_bf16_code(amax0)] + picks
+    codes += [picks[0] if picks else codes[0]] * (width - len(codes))
+    return np.array(codes[:width], np.uint16), len(picks)
+
+
+@pytest.mark.parametrize("amax0,amax1", [(4.3125, 8.25), (2.15625, 5.625), (0.59375, 0.625),
+                                         (10.5, 30.0)])
+def test_append_fp8_growth_by_any_ratio_matches_exact_rounding(amax0, amax1):
+    """Requantisation of the earlier token when the page scale grows by a
+    ratio that is no power of two: each code equals enc(fl32(fl32(dec(c) *
+    s0) / s)), computed in exact arithmetic with each fp32 step rounded once;
+    token 0 holds values for which the other association, enc(fl32(dec(c) *
+    fl32(s0 / s))), gives another code, so this pin tells them apart."""
+    P, Hkv, d = 16, 2, 64
+    bt, (k, v, ks, vs) = _one_seq(P, Hkv, d)
+    x0, n_disc = _discriminating_token(Fraction(amax0), Fraction(amax1), Hkv * d)
+    assert n_disc > 0, "no E4M3 code separates the two associations for this ratio"
+    g = torch.Generator().manual_seed(int(amax1 * 64))
+    x1 = _bf16(torch.randn(1, Hkv, d, generator=g)).reshape(-1)
+    x1 = np.where(np.arange(x1.size) == 0, np.uint16(_bf16_code(Fraction(amax1))), x1)
+    x1 = np.where(np.abs(_bf16_f32(x1)) > amax1, np.uint16(0), x1).astype(np.uint16)
+    t0 = x0.reshape(1, Hkv, d)
+    t1 = x1.reshape(1, Hkv, d)
+    for t, tok in enumerate((t0, t1)):
+        assert oracle.kv_append(tok, tok.copy(), bt, np.array([t + 1], np.int32), k, v,
+                                kv_dtype=1, page_size=P, k_scales=ks, v_scales=vs) == 0
+    page = bt[0, 0]
+    re0, c1, s, alt0 = _exact_two_token_page(x0, x1)
+    assert re0 != alt0
+    for pool, scales, slot_of in ((k, ks, _k_slot), (v, vs, _v_slot)):
+        assert Fraction(float(scales[page])) == s
+        assert slot_of(pool, page, 0).reshape(-1).tolist() == re0
+        assert slot_of(pool, page, 1).reshape(-1).tolist() == c1

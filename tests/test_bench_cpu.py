@@ -2,7 +2,8 @@
 bench.py reports is the decode kernel's FETCH_SIZE and WRITE_SIZE counters,
 each scaled by what the same counter reads for a copy of known size.  These
 tests feed synthetic counter files through the summary and check the
-calibration pick and the scaling against hand-computed values."""
+calibration pick and the scaling against hand-computed values, and do the
+same for the compute-side counter summary (busy fractions, per-step counts)."""
 import csv
 import json
 import os
@@ -72,3 +73,63 @@ def test_missing_decode_dispatches_are_an_error(counters):
     _write(t / "w", [_row(bench.CALIBRATION_KERNEL, "WRITE_SIZE", 1.0)])
     with pytest.raises(ValueError):
         bench.summarize_pmc(str(t / "f"), str(t / "w"), str(t / "l2"), "rollout7b")
+
+
+def _write_compute(d, rows, gpu=("8", "256", "1024", "2400")):
+    os.makedirs(d, exist_ok=True)
+    with open(os.path.join(d, "run_agent_info.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Agent_Type", "Num_Xcc", "Cu_Count", "Simd_Count",
+                                          "Max_Engine_Clk_Fcompute"])
+        w.writeheader()
+        w.writerow({"Agent_Type": "CPU", "Num_Xcc": "0", "Cu_Count": "0", "Simd_Count": "0",
+                    "Max_Engine_Clk_Fcompute": "0"})
+        w.writerow(dict(zip(["Agent_Type", "Num_Xcc", "Cu_Count", "Simd_Count",
+                             "Max_Engine_Clk_Fcompute"], ("GPU",) + gpu)))
+    with open(os.path.join(d, "run_counter_collection.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Counter_Name", "Counter_Value",
+                                          "Start_Timestamp", "End_Timestamp"])
+        w.writeheader()
+        for r in rows:
+            w.writerow(r)
+
+
+def _crow(kernel, counter, value, t0=0, t1=100000):
+    return {"Kernel_Name": kernel, "Counter_Name": counter, "Counter_Value": value,
+            "Start_Timestamp": t0, "End_Timestamp": t1}
+
+
+def test_compute_counters_give_busy_fractions_and_per_step_counts(tmp_path, monkeypatch):
+    """Busy fractions are counter cycles over (GRBM cycles per XCC x SIMDs),
+    quad-cycle counters are scaled by 4, and per-step figures divide by the
+    workload's (page, KV head) steps; other libraries' kernels are left out."""
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path / "profiles"))
+    dec = "void dora::decode_kernel<128, 16, false, 3, false>(dora::DecodeParams)"
+    gui = 8 * 200000.0                         # 200,000 cycles per XCC, two dispatches
+    _write_compute(tmp_path / "c1", [
+        _crow(dec, "GRBM_GUI_ACTIVE", gui, 0, 100000), _crow(dec, "GRBM_GUI_ACTIVE", gui, 0, 100000),
+        _crow(dec, "SQ_INSTS_MFMA", 1200.0), _crow(dec, "SQ_INSTS_MFMA", 1200.0),
+        _crow(dec, "SQ_VALU_MFMA_BUSY_CYCLES", 0.1 * 200000 * 1024),
+        _crow(dec, "SQ_WAVE_CYCLES", 1000.0),
+        _crow("void at::native::elementwise_kernel<4>", "SQ_INSTS_MFMA", 5.0)])
+    _write_compute(tmp_path / "c2", [
+        _crow(dec, "GRBM_GUI_ACTIVE", gui), _crow(dec, "SQ_ACTIVE_INST_VALU", 0.05 * 200000 * 1024),
+        _crow(dec, "SQ_WAIT_ANY", 600.0), _crow(dec, "SQ_LDS_BANK_CONFLICT", 0.0)])
+    _write_compute(tmp_path / "c3", [_crow(dec, "VmemLatency", 2000.0)])
+    bench.summarize_compute([str(tmp_path / c) for c in ("c1", "c2", "c3")], "rollout7b")
+    s = json.load(open(bench.compute_path("rollout7b")))
+    assert list(s["kernels"]) == [dec]
+    k = s["kernels"][dec]
+    assert k["dispatches"] == 2 and k["avg_duration_us"] == pytest.approx(100.0)
+    d = k["derived"]
+    assert d["engine_clock_ghz"] == pytest.approx(2.0)         # 200,000 cycles in 100 us
+    assert d["mfma_busy_frac"] == pytest.approx(0.1)
+    assert d["valu_busy_frac"] == pytest.approx(0.2)           # quad cycles x 4
+    assert d["wave_wait_any_frac"] == pytest.approx(0.6)
+    assert d["vmem_latency_cycles"] == pytest.approx(2000.0)
+    w = wl.BY_NAME["rollout7b"]
+    L = wl.sample_lengths(w, wl.seeds(wl.WORKLOADS.index(w))[0])
+    steps = int(wl.pages_needed(L, w.page_size).sum()) * w.num_kv_heads
+    assert d["steps_per_launch"] == steps
+    assert d["mfma_per_step"] == pytest.approx(1200.0 / steps)
+    assert s["device"] == {"cus": 256, "simds": 1024, "xcc": 8, "max_engine_clock_mhz": 2400}
+    assert s["kernel_source_hash"] == bench.kernel_source_hash()

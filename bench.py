@@ -47,6 +47,9 @@ CALIBRATION_BYTES = 2 << 30                        # read and written per dispat
 TRACE_CMD = ("cd /tmp && rocprofv3 --kernel-trace --stats --output-format csv "
              "-d $REPO/gpurun_out/prof_trace_{w} -o run -- python $REPO/bench.py --only-main "
              "--workload {w} --no-cpu-baseline --steps 30")
+BENCH_TRACE_CMD = ("cd /tmp && rocprofv3 --kernel-trace --stats --output-format csv "
+                   "-d $REPO/gpurun_out/prof_trace_bench -o run -- python $REPO/bench.py "
+                   "> $REPO/gpurun_out/prof_trace_bench.json")
 GRPO_TRACE_CMD = ("cd /tmp && rocprofv3 --kernel-trace --stats --output-format csv "
                   "-d $REPO/gpurun_out/prof_trace_grpo7b -o run -- python $REPO/bench.py "
                   "--grpo-only --steps 30")
@@ -103,6 +106,9 @@ def parse():
                     help="write the kernel-trace summary of a --grpo-only rocprofv3 run")
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="write the kernel-trace summary of a rocprofv3 run under profiles/")
+    ap.add_argument("--summarize-bench-trace", nargs=2, metavar=("DIR", "JSON"),
+                    help="write the kernel-trace summary of a default bench run under "
+                         "rocprofv3, beside the bench line that run printed")
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "L2_DIR"),
                     help="write the HBM-traffic and L2 hit-rate summary of three "
                          "rocprofv3 --pmc runs")
@@ -154,6 +160,65 @@ def summarize_trace(d, workload, grpo=False):
         lines.append(f"| `{name[:70]}` | {r['Calls']} | {avg:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
     lines += ["", f"Kernel source hash: `{kernel_source_hash()}`", ""]
+    os.makedirs(PROFILES, exist_ok=True)
+    open(out, "w").write("\n".join(lines))
+    print(out)
+
+
+def _kernel_instance(w):
+    """Template instance of the decode kernel that workload w launches."""
+    return (f"decode_kernel<{w.head_dim}, {w.page_size}, "
+            f"{'true' if w.kv_dtype == 1 else 'false'}, 3, false>")
+
+
+def summarize_bench_trace(d, line_path):
+    """Kernel-trace summary of the default bench command run under rocprofv3,
+    set beside the event timings of the bench line that same run printed.
+    A decode-kernel instance launched by one workload only (the headline's fp8
+    instance) gives a trace average directly comparable with that workload's
+    event average; an instance shared by several workloads averages over all
+    of their dispatches."""
+    import csv
+    line = json.loads([ln for ln in open(line_path) if ln.strip().startswith("{")][-1])
+    rows = list(csv.DictReader(open(_find_csv(d, "kernel_stats.csv"))))
+    stats = {}
+    for r in rows:
+        name = r.get("Name") or r.get("KernelName") or ""
+        stats[name] = (int(r["Calls"]), float(r.get("AverageNs") or r.get("AvgNs")) / 1e3)
+    by_inst = {}
+    for w in wl.WORKLOADS:
+        if w.name in line.get("workloads", {}):
+            by_inst.setdefault(_kernel_instance(w), []).append(w.name)
+    shared_with_grpo = set()
+    if "shared_prefix" in line:       # the GRPO batch's plain decode, timed as a whole call
+        shared_with_grpo.add(_kernel_instance(wl.GRPO_WORKLOAD))
+    out = os.path.join(PROFILES, f"decode_kernel_{MAIN_WORKLOAD}_bench_trace.md")
+    lines = [f"# rocprofv3 kernel trace of the default bench run (headline: {MAIN_WORKLOAD})",
+             "", "Command (repo root as $REPO):", "", "    " + BENCH_TRACE_CMD, "",
+             "Decode-kernel instances in `run_kernel_stats.csv` (all dispatches of the run),",
+             "beside the event average (`roofline.avg_launch_ms`) that the bench line of",
+             "the same run reports for each workload launching that instance.", "",
+             "| kernel instance | workloads | calls | trace avg us | event avg us | events / trace |",
+             "|---|---|---|---|---|---|"]
+    for inst, names in by_inst.items():
+        hit = [(k, v) for k, v in stats.items() if inst in k]
+        if not hit:
+            continue
+        calls, tavg = hit[0][1]
+        ev = [line["workloads"][n]["roofline"]["avg_launch_ms"] * 1e3 for n in names]
+        shown = names + (["grpo7b (plain path)"] if inst in shared_with_grpo else [])
+        if len(shown) == 1:
+            ratio = f"{ev[0] / tavg:.3f}"
+        else:
+            ratio = "(shared instance)"
+        lines.append(f"| `{inst}` | {', '.join(shown)} | {calls} | {tavg:.2f} | "
+                     f"{', '.join(f'{e:.2f}' for e in ev)} | {ratio} |")
+    rl = line["roofline"]
+    lines += ["", f"Bench line of the run: value {line['value']:.0f} {line['unit']}, "
+              f"{line['ms_per_step'] * 1e3:.1f} us per step; roofline achieved "
+              f"{rl['achieved']:.0f} GB/s, frac {rl['frac']:.3f} "
+              f"({rl['algorithmic_bytes_per_launch']} B per launch).", "",
+              f"Kernel source hash: `{kernel_source_hash()}`", ""]
     os.makedirs(PROFILES, exist_ok=True)
     open(out, "w").write("\n".join(lines))
     print(out)
@@ -729,6 +794,9 @@ def main():
     EVENT_FLAGS = args.event_flags
     if args.summarize_compute:
         summarize_compute(args.summarize_compute[1:], args.summarize_compute[0])
+        return
+    if args.summarize_bench_trace:
+        summarize_bench_trace(*args.summarize_bench_trace)
         return
     if args.summarize_trace or args.summarize_pmc or args.summarize_grpo_trace:
         if args.summarize_grpo_trace:

@@ -133,3 +133,29 @@ def test_compute_counters_give_busy_fractions_and_per_step_counts(tmp_path, monk
     assert d["mfma_per_step"] == pytest.approx(1200.0 / steps)
     assert s["device"] == {"cus": 256, "simds": 1024, "xcc": 8, "max_engine_clock_mhz": 2400}
     assert s["kernel_source_hash"] == bench.kernel_source_hash()
+
+
+def test_bench_trace_sets_trace_beside_events(tmp_path, monkeypatch):
+    """The default-run trace summary pairs each decode-kernel instance with the
+    workloads that launch it and, for an instance of one workload only, gives
+    the ratio of that workload's event average to the trace average."""
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path / "profiles"))
+    d = tmp_path / "t"
+    os.makedirs(d)
+    with open(d / "run_kernel_stats.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Name", "Calls", "AverageNs", "MinNs", "MaxNs"])
+        w.writeheader()
+        w.writerow({"Name": "void dora::decode_kernel<128, 32, true, 3, false>(dora::DecodeParams)",
+                    "Calls": 65, "AverageNs": 2000000.0, "MinNs": 1, "MaxNs": 2})
+        w.writerow({"Name": "void dora::decode_kernel<128, 16, false, 3, false>(dora::DecodeParams)",
+                    "Calls": 260, "AverageNs": 100000.0, "MinNs": 1, "MaxNs": 2})
+    rl = lambda ms: {"roofline": {"avg_launch_ms": ms}}
+    line = {"value": 1.0, "unit": "tokens/s", "ms_per_step": 2.1,
+            "roofline": {"achieved": 1.0, "frac": 0.5, "algorithmic_bytes_per_launch": 7},
+            "workloads": {"moe_fp8": rl(2.02), "rollout7b": rl(0.1), "tail_only": rl(0.17)}}
+    (tmp_path / "line.json").write_text("[bench] noise\n" + json.dumps(line) + "\n")
+    bench.summarize_bench_trace(str(d), str(tmp_path / "line.json"))
+    text = open(os.path.join(bench.PROFILES, f"decode_kernel_{bench.MAIN_WORKLOAD}_bench_trace.md")).read()
+    assert "| `decode_kernel<128, 32, true, 3, false>` | moe_fp8 | 65 | 2000.00 | 2020.00 | 1.010 |" in text
+    assert "rollout7b, tail_only" in text and "(shared instance)" in text
+    assert bench.BENCH_TRACE_CMD in text

@@ -40,6 +40,7 @@ import workloads as wl  # noqa: E402
 METRIC = "decode-attn tokens/s and HBM GB/s (% of peak) on long-tail length mixes"
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 MAIN_WORKLOAD = "moe_fp8"
+SINGLE_CORE_WORKLOADS = ("tiny", "rollout7b")   # the oracle on one core as well
 PROFILES = os.path.join(ROOT, "profiles")
 DECODE_KERNEL = "dora::decode_kernel"
 CALIBRATION_KERNEL = "__amd_rocclr_copyBuffer"   # the 2 GiB device copy in copy_bandwidth()
@@ -691,16 +692,20 @@ def stream_read_reference(torch, dora, flush, steps=10, buf_bytes=8 << 30, read_
     return out
 
 
-def cpu_baseline(b, budget_s=20.0, min_s=10.0):
+def cpu_baseline(b, budget_s=20.0, min_s=10.0, threads=None):
     """The fp64 oracle on the host cores over the same batch (or a prefix of
     its sequences that fits the time budget), repeated until min_s of work is
-    timed, scaled to decode tokens/s.  Threads: OMP_NUM_THREADS when set (the
-    host's CPU share for this GPU), else every core in the affinity mask."""
+    timed, scaled to decode tokens/s.  Threads: `threads` when given, else
+    OMP_NUM_THREADS when set (the host's CPU share for this GPU), else every
+    core in the affinity mask."""
     import oracle
 
     mask = len(os.sched_getaffinity(0))
     env = os.environ.get("OMP_NUM_THREADS", "")
-    cores = min(mask, int(env)) if env.isdigit() and int(env) > 0 else mask
+    if threads:
+        cores = threads
+    else:
+        cores = min(mask, int(env)) if env.isdigit() and int(env) > 0 else mask
     order = list(range(b.w.num_seqs))
     # calibrate on one sequence, then take as many sequences as the budget allows
     probe = wl.subset_for_oracle(b, order[:1])
@@ -737,7 +742,8 @@ def cpu_baseline(b, budget_s=20.0, min_s=10.0):
                       f"run {reps} times ({total:.1f} s, {dt:.3f} s each), scaled by "
                       f"total/sampled context tokens",
             "affinity_mask_cores": mask,
-            "threads_source": "OMP_NUM_THREADS" if cores != mask or env else "affinity mask",
+            "threads_source": ("fixed" if threads else
+                               "OMP_NUM_THREADS" if cores != mask or env else "affinity mask"),
             "cpu_model": _cpu_model()}
 
 
@@ -853,6 +859,9 @@ def main():
         rec["split_kernel_traffic_bytes"] = pmc["traffic_bytes_per_launch"] if pmc else None
         rec["split_kernel_l2_hit_rate"] = pmc["l2"]["decode_kernel"]["hit_rate"] if pmc else None
         rec["append"] = time_append(torch, dora, b, max(5, steps // 2), flush)
+        if name in SINGLE_CORE_WORKLOADS and not args.no_cpu_baseline:
+            log(f"workload {name}: single-core oracle")
+            rec["cpu_baseline_1core"] = cpu_baseline(b, budget_s=6.0, min_s=3.0, threads=1)
         if w.pack_seqs:
             log(f"workload {name}: pack/unpack")
             rec["pack_unpack"] = time_pack(torch, dora, b, max(5, steps // 2), flush)

@@ -28,7 +28,9 @@
  *     this ABI.  Device-data errors (a page id outside the pool, a page not
  *     owned by the sequence's version, seq_lens[b] > block_table_stride *
  *     page_size) are undefined behaviour unless DORA_FLAG_VALIDATE is set.
- *   - No global mutable state; pool objects are single-threaded.
+ *   - No global mutable state, with one exception: the fixed per-GPU
+ *     workspace of dora_decode_attn_noalloc (calls of that entry point that
+ *     overlap on one GPU race on it).  Pool objects are single-threaded.
  *
  * Data layouts (row-major, innermost index last; e = 2 bytes for bf16, 1 for
  * fp8; X = 16 / e, i.e. one 16-byte chunk of the head dimension):

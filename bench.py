@@ -655,16 +655,16 @@ def copy_bandwidth(torch, nbytes=2 << 30):
     return rate
 
 
-def stream_read_reference(torch, dora, flush, steps=10, buf_bytes=8 << 30, read_bytes=1 << 30,
+def stream_read_reference(torch, dora, flush, steps=6, buf_bytes=16 << 30, read_bytes=4 << 30,
                           tile=4096):
     """Achievable read bandwidth with the decode kernel's access pattern: the
-    library's streaming-read kernel (dora_stream_read) over 1 GiB of 4 KiB
-    tiles of an 8 GiB buffer, in random or in sequential order, swept over
-    the wavefronts per CU (5, as the decode launches for bf16 pages, and 8,
-    every resident slot, as for fp8 pages) and the tiles each wavefront keeps
-    per batch (1, 2 or 4, two batches in flight).  Median of `steps` calls per
-    variant, caches evicted before each; achievable_gbps is the best random
-    variant."""
+    library's streaming-read kernel (dora_stream_read) over 4 GiB of 4 KiB
+    tiles of a 16 GiB buffer (long enough that launch and ramp-down cost under
+    1%), in random or in sequential order, swept over the wavefronts per CU
+    (5, as the decode launches for bf16 pages; 8, every resident slot, as for
+    fp8 pages; 12 and 16) and the tiles each wavefront keeps per batch (1, 2
+    or 4, two batches in flight).  Median of `steps` calls per variant, caches
+    evicted before each; achievable_gbps is the best random variant."""
     props = torch.cuda.get_device_properties(0)
     cus = props.multi_processor_count
     buf = torch.empty(buf_bytes, dtype=torch.uint8, device="cuda")
@@ -677,7 +677,7 @@ def stream_read_reference(torch, dora, flush, steps=10, buf_bytes=8 << 30, read_
            "gbps": {}}
     for name, ids in orders.items():
         tiles = torch.from_numpy(ids).cuda()
-        for per_cu in (5, 8):
+        for per_cu in (5, 8, 12, 16):
             sink = torch.zeros(cus * per_cu, dtype=torch.int32, device="cuda")
             for tpb in (1, 2, 4):
                 ts = time_calls(torch, lambda: dora.dora_stream_read(

@@ -113,8 +113,15 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   constexpr int DBLK = D / 16;
   constexpr int E = FP8 ? 1 : 2;
   constexpr int TILE_BYTES = P * D * E;  // one KV head of one page
-  // next-segment query prefetch, where the register budget allows it
-  constexpr bool QPF = !(P == 32 && !FP8 && D == 128);
+  // Query operands.  bf16 pages: each page buffer carries the query operand
+  // of its own (b, g), loaded with the page, so a page's first MFMA never
+  // waits on a load issued after the next pages' (a query load under a
+  // branch would be waited for together with everything issued before it).
+  // fp8 pages: one operand per segment, the next segment's fetched with its
+  // first page; the extra query loads of the per-page form cost the fp8
+  // kernel more than its waits (measured: bf16 batches 0.5-1.2% faster with
+  // per-page operands, the fp8 batch 2% slower).
+  constexpr bool QSLOT = !FP8;
   extern __shared__ int sN[];            // page prefix over sequences, [B + 1]
 
   const int lane = threadIdx.x;
@@ -227,7 +234,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
 
   // running state of the current segment
   f32x4 acc[DBLK];
-  bf16x8 qop[KSTEPS];
+  bf16x8 qop[QSLOT ? 1 : KSTEPS];
   float m_run = -__builtin_inff(), l_run = 0.f;
   int seg_b = 0, seg_g = 0;
   bool seg_whole = false, seg_here = false, first_seg = true;
@@ -238,9 +245,10 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   auto load_q = [&](bf16x8(&dst)[KSTEPS], int b, int g) {
     load_q_operand<D, FP8>(dst, p.q + ((int64_t)b * Hq + (int64_t)g * G + col) * D, col < G);
   };
-  // The query of the next segment is fetched together with that segment's
-  // first page (q_next, tagged with the page-head where the segment starts).
-  bf16x8 q_next[QPF ? KSTEPS : 1];
+  // fp8: the query of the next segment is fetched together with that
+  // segment's first page (q_next, tagged with the page-head where the
+  // segment starts).
+  bf16x8 q_next[QSLOT ? 1 : KSTEPS];
   int q_next_at = -1;
 
   auto start_segment = [&](int b, int g, bool whole, int x) {
@@ -252,12 +260,14 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
     l_run = 0.f;
 #pragma unroll
     for (int i = 0; i < DBLK; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (x == x0) return;  // the range's first query was loaded up front
-    if (QPF && q_next_at == x) {
+    if constexpr (!QSLOT) {
+      if (x == x0) return;  // the range's first query was loaded up front
+      if (q_next_at == x) {
 #pragma unroll
-      for (int s = 0; s < (QPF ? KSTEPS : 1); ++s) qop[s] = q_next[s];
-    } else {
-      load_q(qop, b, g);  // a second segment start inside the prefetch window
+        for (int s = 0; s < KSTEPS; ++s) qop[s] = q_next[s];
+      } else {
+        load_q(qop, b, g);  // a second segment start inside the prefetch window
+      }
     }
   };
 
@@ -302,8 +312,8 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
     first_seg = false;
   };
 
-  auto consume = [&](const R& r, int nvalid, float ksc, float vsc) {
-    consume_page<D, P, FP8>(r, nvalid, ksc, vsc, qop, acc, m_run, l_run);
+  auto consume = [&](const R& r, const bf16x8(&qo)[KSTEPS], int nvalid, float ksc, float vsc) {
+    consume_page<D, P, FP8>(r, nvalid, ksc, vsc, qo, acc, m_run, l_run);
   };
 
   // 3. stream the range.  Descriptors come in chunks of 64 (current and next);
@@ -317,6 +327,7 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   asm volatile("" ::"v"(bt_sink));  // keeps the table prefetch
 
   R buf[NBUF];
+  bf16x8 qb[QSLOT ? NBUF : 1][KSTEPS];  // bf16: each page's query operand
   int s_b[NBUF];
   uint32_t s_info[NBUF];
   float s_ks[NBUF], s_vs[NBUF];
@@ -340,11 +351,11 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
     const uint32_t info = (uint32_t)__builtin_amdgcn_readlane((int)cb_info, i);
     s_b[r] = b;
     s_info[r] = info;
-    if constexpr (QPF) {
-      if (desc_j(info) == 0 && x > x0 && x > q_next_at) {
-        load_q(q_next, b, desc_g(info));
-        q_next_at = x;
-      }
+    if constexpr (QSLOT) {
+      load_q(qb[r], b, desc_g(info));
+    } else if (desc_j(info) == 0 && x > x0 && x > q_next_at) {
+      load_q(q_next, b, desc_g(info));
+      q_next_at = x;
     }
     const int64_t tile = (int64_t)pid * pb + (int64_t)desc_g(info) * TILE_BYTES;
     if constexpr (FP8) {
@@ -358,8 +369,9 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
                          past ? 0u : voff);
   };
 
-  load_q(qop, __builtin_amdgcn_readlane(cb_b, 0),
-         desc_g((uint32_t)__builtin_amdgcn_readlane((int)cb_info, 0)));
+  if constexpr (!QSLOT)
+    load_q(qop, __builtin_amdgcn_readlane(cb_b, 0),
+           desc_g((uint32_t)__builtin_amdgcn_readlane((int)cb_info, 0)));
 #pragma unroll
   for (int k = 0; k < NBUF - 1; ++k) prefetch(k, x0 + k);
   int x = x0;
@@ -370,7 +382,10 @@ __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
       const uint32_t info = s_info[r];
       const int j = desc_j(info);
       if (x == x0 || j == 0) start_segment(s_b[r], desc_g(info), j == 0, x);
-      consume(buf[r], desc_nvalid(info), s_ks[r], s_vs[r]);
+      if constexpr (QSLOT)
+        consume(buf[r], qb[r], desc_nvalid(info), s_ks[r], s_vs[r]);
+      else
+        consume(buf[r], qop, desc_nvalid(info), s_ks[r], s_vs[r]);
       if (desc_last(info) || x == x1 - 1) {
         seg_whole = seg_whole && desc_last(info);
         finish_segment();

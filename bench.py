@@ -692,6 +692,49 @@ def stream_read_reference(torch, dora, flush, steps=6, buf_bytes=16 << 30, read_
     return out
 
 
+def pattern_tiles(w, lengths, block_table_h):
+    """The K and V tiles a decode of this batch reads, in the order of its work
+    list ((sequence, KV head, page) page-heads, each one's K tile then its V
+    tile), as tile indices into one buffer laid out [K pool][V pool] with the
+    pools' own layout: tile (page, head) at page * Hkv + head."""
+    H = w.num_kv_heads
+    n = wl.pages_needed(lengths, w.page_size)
+    parts = []
+    for b, nb in enumerate(n):
+        pids = block_table_h[b, :nb].astype(np.int64)
+        for g in range(H):
+            k = pids * H + g
+            parts.append(np.stack([k, k + w.num_pages * H], 1).reshape(-1))
+    ids = np.concatenate(parts) if parts else np.zeros(0, np.int64)
+    return ids.astype(np.int32)
+
+
+def pattern_reference(torch, dora, w, lengths, block_table_h, decode_waves, flush, steps=6):
+    """Achievable read rate for this batch's exact access pattern: the
+    streaming-read kernel over the tiles the decode reads, in its order,
+    split in equal contiguous ranges over the decode's own wavefront count
+    and over 8 per CU, with 2 or 4 tiles per batch.  The buffer holds a K pool
+    and a V pool of the batch's geometry (contents irrelevant)."""
+    tile = w.page_size * w.head_dim * (1 if w.kv_dtype == 1 else 2)
+    ids = pattern_tiles(w, lengths, block_table_h)
+    buf = torch.empty(2 * w.num_pages * w.num_kv_heads * tile, dtype=torch.uint8, device="cuda")
+    tiles = torch.from_numpy(ids).cuda()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    out = {"tile_bytes": tile, "tiles": int(len(ids)), "gbps": {}}
+    for waves in sorted({int(decode_waves), 8 * cus}):
+        sink = torch.zeros(waves, dtype=torch.int32, device="cuda")
+        for tpb in (2, 4):
+            ts = time_calls(torch, lambda: dora.dora_stream_read(
+                buf, tiles, sink, tile_bytes=tile, tiles_per_batch=tpb), steps, 2, flush)
+            ms = float(np.median(ts))
+            out["gbps"][f"{waves}_waves_{tpb}_tiles"] = len(ids) * tile / (ms * 1e-3) / 1e9
+    best = max((v, k) for k, v in out["gbps"].items())
+    out["best_gbps"], out["best_variant"] = best
+    del buf, tiles
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(b, budget_s=20.0, min_s=10.0, threads=None):
     """The fp64 oracle on the host cores over the same batch (or a prefix of
     its sequences that fits the time budget), repeated until min_s of work is
@@ -774,10 +817,13 @@ def load_pmc(w):
 def roofline_of(rec, achievable_gbps):
     """Roofline object of one workload's decode kernel: algorithmic bytes per
     launch over the kernel's average duration by events; traffic from the
-    committed counter summary when it matches the kernel sources."""
+    committed counter summary when it matches the kernel sources; the
+    fraction of the generic streaming-read reference and of the reference on
+    this batch's own access pattern."""
     ab = rec["algorithmic_bytes"]["total"]
     ms = rec["split_kernel_ms"]
     gbps = ab / (ms * 1e-3) / 1e9
+    pat = rec.get("pattern_reference")
     return {
         "bound": "hbm",
         "kernel": "decode_kernel",
@@ -791,6 +837,8 @@ def roofline_of(rec, achievable_gbps):
         "avg_launch_ms": ms,
         "achievable_gbps": achievable_gbps,
         "frac_of_achievable": gbps / achievable_gbps,
+        "pattern_gbps": pat["best_gbps"] if pat else None,
+        "frac_of_pattern": gbps / pat["best_gbps"] if pat else None,
     }
 
 
@@ -868,6 +916,11 @@ def main():
         results[name] = rec
         log(f"workload {name}: {rec['ms_per_step']:.4f} ms/step, "
             f"{rec['hbm_gbps']:.0f} GB/s, split kernel {rec['split_kernel_gbps']:.0f} GB/s")
+        lengths, table_h = b.lengths, b.block_table_h
+        waves = dora.dora_decode_num_waves(dora.make_decode_desc(
+            num_seqs=w.num_seqs, num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads,
+            head_dim=w.head_dim, page_size=w.page_size, block_table_stride=b.stride,
+            num_pages=w.num_pages, kv_dtype=w.kv_dtype, num_waves=args.num_waves))
         if name == args.workload:
             main_rec, main_w = rec, w
             main_rec["steps_wall_s"] = t["wall_s"]
@@ -876,6 +929,10 @@ def main():
                 cpu = cpu_baseline(b)
         del b, t
         torch.cuda.empty_cache()
+        if name != "tiny":
+            log(f"workload {name}: reference read of its access pattern")
+            rec["pattern_reference"] = pattern_reference(torch, dora, w, lengths, table_h,
+                                                         waves, flush)
 
     grpo = None
     if not args.only_main:

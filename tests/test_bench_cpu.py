@@ -8,6 +8,7 @@ import csv
 import json
 import os
 
+import numpy as np
 import pytest
 
 import bench
@@ -159,3 +160,22 @@ def test_bench_trace_sets_trace_beside_events(tmp_path, monkeypatch):
     assert "| `decode_kernel<128, 32, true, 3, false>` | moe_fp8 | 65 | 2000.00 | 2020.00 | 1.010 |" in text
     assert "rollout7b, tail_only" in text and "(shared instance)" in text
     assert bench.BENCH_TRACE_CMD in text
+
+
+def test_pattern_tiles_follow_the_decode_work_order():
+    """The exact-pattern reference reads, for every (sequence, KV head, page)
+    page-head in that order, the K tile then the V tile at the byte offsets the
+    pools' layout gives them (page * Hkv + head tiles into the pool; the V
+    pool after the K pool)."""
+    w = wl.Workload("t", 3, 4, 2, 64, 16, 0, 64, "lognormal", 40, 1.0, 1, 100)
+    lengths = np.array([33, 0, 16], np.int32)
+    table = np.array([[5, 9, 2], [0, 0, 0], [7, 0, 0]], np.int32)
+    ids = bench.pattern_tiles(w, lengths, table)
+    want = []
+    for b, L in enumerate(lengths):
+        for g in range(w.num_kv_heads):
+            for j in range(-(-int(L) // w.page_size)):
+                pid = int(table[b, j])
+                want += [pid * 2 + g, w.num_pages * 2 + pid * 2 + g]
+    assert ids.tolist() == want
+    assert ids.dtype == np.int32 and ids.max() < 2 * w.num_pages * w.num_kv_heads

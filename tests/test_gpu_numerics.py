@@ -1,0 +1,82 @@
+"""Numerical corner cases of dora_decode_attn through the C ABI, against the
+fp64 oracle and closed forms: a caller-set softmax scale, scores large enough
+that all but a few weights underflow, and a zero query (every weight equal,
+so the output is the plain mean of the values)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+from gpu_util import TOL, gpu_batch, max_abs_err, oracle_for, run_decode
+
+pytestmark = pytest.mark.gpu
+
+LENS = np.array([1, 17, 300, 2049, 0, 64, 5000, 33], np.int32)
+
+
+def _w(d, P, dt, G=8, Hkv=2):
+    pages = int(wl.pages_needed(LENS, P).sum()) * 2 + 8
+    return wl.Workload("n", len(LENS), G * Hkv, Hkv, d, P, dt, pages, "uniform", lo=1, hi=1)
+
+
+def _oracle(b, scale):
+    s = wl.subset_for_oracle(b, list(range(b.w.num_seqs)))
+    return oracle.decode(s["q"], s["k_pages"], s["v_pages"], s["block_table"], s["seq_lens"],
+                         num_kv_heads=b.w.num_kv_heads, page_size=b.w.page_size,
+                         kv_dtype=b.w.kv_dtype, scale=scale, k_scales=s["k_scales"],
+                         v_scales=s["v_scales"], num_pages=s["num_pages"])
+
+
+@pytest.mark.parametrize("dt,P", [(0, 16), (1, 32)])
+@pytest.mark.parametrize("scale", [0.03, 1.0])
+def test_caller_softmax_scale(dt, P, scale):
+    print(f"[case] sm_scale {scale} dt={dt} P={P}", flush=True)
+    b = gpu_batch(_w(128, P, dt), lengths=LENS, seed_index=300 + dt)
+    out = run_decode(b, sm_scale=scale)
+    err = max_abs_err(out, _oracle(b, scale))
+    assert err <= TOL[dt], err
+
+
+@pytest.mark.parametrize("dt,P", [(0, 16), (1, 32)])
+def test_large_scores_underflow_safely(dt, P):
+    """q scaled by 24: scores of a few hundred, so exp() of most tokens'
+    scores relative to the maximum underflows to zero; the online softmax must
+    still give the oracle's nearly one-hot mixture, with no NaN or infinity."""
+    print(f"[case] large scores dt={dt} P={P}", flush=True)
+    b = gpu_batch(_w(128, P, dt), lengths=LENS, seed_index=310 + dt)
+    b.q.copy_((b.q.float() * 24).to(torch.bfloat16))
+    out = run_decode(b)
+    err = max_abs_err(out, oracle_for(b))
+    assert err <= TOL[dt], err
+
+
+@pytest.mark.parametrize("dt,P", [(0, 16), (1, 32)])
+def test_zero_query_is_the_mean_of_values(dt, P):
+    """With q = 0 every score is 0 and the output is the mean of the
+    sequence's value rows: checked against a direct mean of the stored values,
+    computed here from the page layout with no attention code."""
+    print(f"[case] zero query dt={dt} P={P}", flush=True)
+    w = _w(64, P, dt)
+    b = gpu_batch(w, lengths=LENS, seed_index=320 + dt)
+    b.q.zero_()
+    out = run_decode(b).float().cpu().numpy()
+    G = w.num_q_heads // w.num_kv_heads
+    vp = b.v_pages.cpu()
+    vp = (vp.view(torch.float8_e4m3fn).float() if dt == 1 else vp.float()).numpy()
+    vs = b.v_scales.cpu().numpy() if dt == 1 else None
+    bt = b.block_table_h
+    for s, L in enumerate(LENS):
+        for g in range(w.num_kv_heads):
+            if L == 0:
+                assert np.all(out[s, g * G:(g + 1) * G] == 0)
+                continue
+            rows = []
+            for t in range(L):
+                p = int(bt[s, t // P])
+                v = vp[p, g, :, t % P] * (vs[p] if dt == 1 else 1.0)   # [d], V stored [d][P]
+                rows.append(v)
+            mean = np.mean(np.stack(rows), axis=0)
+            for h in range(G):
+                err = np.abs(out[s, g * G + h] - mean).max()
+                assert err <= TOL[dt], (s, g, h, err)

@@ -17,9 +17,14 @@ sequence advances one token per step).  roofline: the decode kernel's
 algorithmic bytes (K and V of valid tokens, page scales, Q, output, block
 table and lengths) over its average duration, measured with HIP events that
 the library records around each kernel on the launch stream
-(dora_decode_attn_timed).  The achievable-bandwidth reference beside the
-8 TB/s peak is the library's own streaming-read kernel (dora_stream_read:
-random 4 KiB tiles, non-temporal loads, the decode kernel's access pattern).
+(dora_decode_attn_timed).  Two achievable-bandwidth references stand beside
+the 8 TB/s peak, both read by the library's own streaming-read kernel
+(dora_stream_read, 16-byte non-temporal loads): random 4 KiB tiles of a
+16 GiB buffer (achievable_gbps), and each batch's own tile sequence in its
+decode work order (pattern_gbps).  traffic: HBM bytes per launch from the
+committed rocprofv3 counter summary, while it matches the kernel sources.
+The rocprofv3 summaries under profiles/ are made from this script's runs
+with the --summarize-* options.
 """
 from __future__ import annotations
 

@@ -3,7 +3,8 @@ is the library's fixed per-GPU array.  Two calls in a row, the second on a
 smaller batch of another geometry, each equal bit for bit to dora_decode_attn
 on the same inputs (same launch, same arithmetic) and within the oracle
 tolerance; sizes beyond the array and the VALIDATE flag are refused before any
-launch; the calls allocate no device memory."""
+launch; the calls allocate no device memory, and a call captured in a HIP
+graph replays equal to the eager call."""
 import numpy as np
 import pytest
 import torch
@@ -75,3 +76,41 @@ def test_noalloc_allocates_no_device_memory():
         _noalloc(b, out=out)
     assert torch.cuda.mem_get_info()[0] == free0
     assert torch.equal(out.view(torch.int16), run_decode(b).view(torch.int16))
+
+
+def test_noalloc_captures_in_a_graph_and_replays_equal_eager():
+    """The callers this entry point is for include code under HIP graph
+    capture: one call captured after a first eager call on the device (which
+    looks the array's address up), then replayed with new queries copied into
+    the captured buffer; every replay equals dora_decode_attn on the same
+    inputs bit for bit, with eager work and a synchronisation between
+    replays."""
+    d = lib()
+    lens = np.array([2000, 1, 0, 517, 64, 3000, 16, 95], np.int32)
+    w = wl.Workload("na5", len(lens), 32, 4, 128, 16, 0, 2048, "uniform", lo=1, hi=1)
+    b = gpu_batch(w, lengths=lens, seed_index=95)
+    kw = dict(num_kv_heads=w.num_kv_heads, page_size=w.page_size, kv_dtype=w.kv_dtype,
+              k_scales=b.k_scales, v_scales=b.v_scales)
+    q_s, out_g = b.q.clone(), torch.empty_like(b.q)
+    _noalloc(b, out=out_g)                         # eager first call on the device
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            d.dora_decode_attn_noalloc(q_s, b.k_pages, b.v_pages, b.block_table, b.seq_lens,
+                                       b.version_ids, out_g, **kw)
+    torch.cuda.current_stream().wait_stream(s)
+    gen = torch.Generator(device="cuda").manual_seed(96)
+    for rep in range(3):
+        print(f"[case] noalloc graph replay {rep}", flush=True)
+        q_new = torch.randn(b.q.shape, generator=gen, device="cuda").to(torch.bfloat16)
+        q_s.copy_(q_new)
+        out_g.fill_(7.0)
+        g.replay()
+        torch.cuda.synchronize()
+        out_e = torch.empty_like(b.q)
+        d.dora_decode_attn(q_new, b.k_pages, b.v_pages, b.block_table, b.seq_lens,
+                           b.version_ids, out_e, **kw)
+        torch.cuda.synchronize()
+        assert torch.equal(out_g.view(torch.int16), out_e.view(torch.int16)), rep

@@ -9,7 +9,6 @@ libdora.so is missing, importing this module raises.
 from __future__ import annotations
 
 import ctypes
-import math
 import os
 from typing import Optional, Sequence
 
@@ -659,6 +658,3 @@ class Pool:
                "dora_pool_migrate_seq")
         return new_id.value, src[:got.value], dstp[:got.value]
 
-
-def default_scale(head_dim: int) -> float:
-    return 1.0 / math.sqrt(head_dim)

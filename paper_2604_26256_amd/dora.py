@@ -657,4 +657,3 @@ class Pool:
                                           dstp.ctypes.data_as(_P), cap, ctypes.byref(got)),
                "dora_pool_migrate_seq")
         return new_id.value, src[:got.value], dstp[:got.value]
-

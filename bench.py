@@ -79,11 +79,23 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2604_26256_amd", "csrc", f)
                   for f in ("decode.hip", "decode_core.h", "dora_internal.h", "api.cpp")]
 
 
+def _code_only(text: str) -> str:
+    """C/C++ source with comments removed and whitespace collapsed, so that a
+    comment edit does not count as a change of the kernels (string literals
+    in these sources hold no comment markers)."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_hash() -> str:
+    """Hash of the code (not the comments) of the sources the decode kernel's
+    launches are built from; stored with every counter summary."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -52,7 +52,7 @@ namespace dora {
 // Decode wavefronts per launch.  bf16 pages take at most kBf16WavesPerCu per
 // CU: past about one wavefront per SIMD the kernel is bound by HBM, and each
 // extra wavefront only adds cuts, partials and combine work (the 7B-class
-// batch is 4-5% faster at 5 per CU than at every resident slot; the larger
+// batch is 2-3% faster per step at 5 per CU than at every resident slot; the larger
 // batches are level).  fp8 pages keep every resident slot: their per-page
 // conversion work needs the occupancy.  Never more than the batch can use:
 // at most B * Hkv * stride page-heads, min_range each.

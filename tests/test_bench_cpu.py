@@ -179,3 +179,9 @@ def test_pattern_tiles_follow_the_decode_work_order():
                 want += [pid * 2 + g, w.num_pages * 2 + pid * 2 + g]
     assert ids.tolist() == want
     assert ids.dtype == np.int32 and ids.max() < 2 * w.num_pages * w.num_kv_heads
+
+
+def test_source_hash_ignores_comments_only():
+    code = "int f(int x) { // add one\n  return x + 1; /* done */ }\n"
+    assert bench._code_only(code) == bench._code_only("int f(int x) {\n return x + 1;  }")
+    assert bench._code_only(code) != bench._code_only("int f(int x) { return x + 2; }")

@@ -396,7 +396,7 @@ def shared_prefix_algorithmic_bytes(w: Workload, lengths: np.ndarray, shared: np
     ab = dict(ab)
     ab["kv"] -= dup
     ab["total"] -= dup
-    ab["shared_kv_counted_once"] = dup
+    ab["duplicate_kv_not_counted"] = dup  # members' re-reads of shared pages
     return ab
 
 

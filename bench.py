@@ -975,7 +975,9 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if w.kv_dtype == 0 else "fp8_e4m3 KV, bf16 Q",
+        # the arithmetic: bf16 MFMA operands, fp32 accumulation and softmax
+        # (fp8 pages are widened to bf16 in registers, exactly)
+        "dtype": "bf16" if w.kv_dtype == 0 else "bf16 (KV stored fp8_e4m3)",
         "data": "synthetic",
         "config": {
             "workload": w.name, "num_seqs": w.num_seqs, "num_q_heads": w.num_q_heads,

@@ -1,7 +1,9 @@
 """Numerical corner cases of dora_decode_attn through the C ABI, against the
 fp64 oracle and closed forms: a caller-set softmax scale, scores large enough
-that all but a few weights underflow, and a zero query (every weight equal,
-so the output is the plain mean of the values)."""
+that all but a few weights underflow, a zero query (every weight equal, so
+the output is the plain mean of the values), and the geometry's limits (a
+very long sequence, the widest KV-head count, the largest block-table
+stride)."""
 import numpy as np
 import pytest
 import torch
@@ -80,3 +82,50 @@ def test_zero_query_is_the_mean_of_values(dt, P):
             for h in range(G):
                 err = np.abs(out[s, g * G + h] - mean).max()
                 assert err <= TOL[dt], (s, g, h, err)
+
+
+@pytest.mark.parametrize("dt,P", [(0, 16), (1, 32)])
+def test_one_sequence_of_half_a_million_tokens(dt, P):
+    """The geometry's far corner: one sequence of 2^19 tokens (2^15 or 2^14
+    pages in one block-table row) over the widest query group (G = 16) of a
+    single KV head, so the one segment is cut across every wavefront of the
+    default launch and the combine merges over a thousand pieces.  A softmax
+    scale of 1 keeps the output dominated by a few tokens (with 1/sqrt(d) the
+    output of half a million random values would be near zero and say
+    little).  The oracle takes about ten seconds per case."""
+    print(f"[case] 2^19 tokens dt={dt} P={P}", flush=True)
+    lens = np.array([1 << 19], np.int32)
+    pages = int(wl.pages_needed(lens, P).sum()) + 8
+    w = wl.Workload("m", 1, 16, 1, 64, P, dt, pages, "uniform", lo=1, hi=1)
+    b = gpu_batch(w, lengths=lens, seed_index=330 + dt)
+    out = run_decode(b, sm_scale=1.0)
+    ref = _oracle(b, 1.0)
+    assert np.abs(ref).max() > 0.5, "the check needs outputs of order one"
+    err = max_abs_err(out, ref)
+    assert err <= TOL[dt], err
+
+
+def test_widest_kv_head_count():
+    """127 KV heads (the descriptor's limit), one query head each."""
+    print("[case] Hkv=127", flush=True)
+    lens = np.array([1, 17, 300, 0, 2049], np.int32)
+    pages = int(wl.pages_needed(lens, 16).sum()) * 2 + 8
+    w = wl.Workload("h", len(lens), 127, 127, 64, 16, 0, pages, "uniform", lo=1, hi=1)
+    b = gpu_batch(w, lengths=lens, seed_index=340)
+    out = run_decode(b)
+    err = max_abs_err(out, oracle_for(b))
+    assert err <= TOL[0], err
+
+
+def test_largest_block_table_stride():
+    """Block-table rows of 2^19 - 1 entries (the descriptor's limit): row
+    offsets past 2^21 bytes, the pages of each sequence at the row's start."""
+    print("[case] stride 2^19-1", flush=True)
+    lens = np.array([1, 500, 33], np.int32)
+    pages = int(wl.pages_needed(lens, 16).sum()) * 2 + 8
+    w = wl.Workload("s", len(lens), 8, 2, 64, 16, 0, pages, "uniform", lo=1, hi=1)
+    b = wl.make_batch(w, device="cuda", seed_index=341, lengths=lens, stride=(1 << 19) - 1)
+    assert b.block_table.shape[1] == (1 << 19) - 1
+    out = run_decode(b)
+    err = max_abs_err(out, oracle_for(b))
+    assert err <= TOL[0], err

@@ -796,8 +796,11 @@ def cpu_baseline(b, budget_s=20.0, min_s=10.0, threads=None):
     ctx = int(b.lengths[take].sum())
     # one decode step of the whole batch costs sum(L) context tokens of work
     step_s = dt * float(b.lengths.sum()) / ctx
-    return {"value": b.w.num_seqs / step_s, "unit": "tokens/s", "cores": cores,
-            "kind": "oracle",
+    # threads that ran: the oracle's parallel loop is over (sequence, KV head)
+    # units, with at most the requested (and OpenMP-available) threads
+    used = min(cores, oracle.max_threads(), len(take) * b.w.num_kv_heads)
+    return {"value": b.w.num_seqs / step_s, "unit": "tokens/s", "cores": used,
+            "threads_requested": cores, "kind": "oracle",
             "sample": f"{len(take)} of {b.w.num_seqs} sequences ({ctx} context tokens), "
                       f"run {reps} times ({total:.1f} s, {dt:.3f} s each), scaled by "
                       f"total/sampled context tokens",

@@ -7,6 +7,8 @@
 * The set of (sequence, KV head) segments a decode launch cuts across
   wavefronts, which the full-size parity tests use, equals a brute-force
   enumeration of the documented equal-range split.
+* The helpers that lay token-major keys and values out as pages follow the
+  C header's page layouts element by element.
 """
 import math
 
@@ -90,3 +92,27 @@ def test_page_chunks_cover_every_sequence_once():
     n = wl.pages_needed(L, 16)
     for r in runs:
         assert len(r) == 1 or n[r].sum() <= 64
+
+
+@pytest.mark.parametrize("kv_dtype,P,H,d", [(0, 16, 2, 64), (1, 32, 3, 128), (0, 32, 1, 128)])
+def test_page_layout_helpers_follow_the_documented_layout(kv_dtype, P, H, d):
+    """The helpers that build pages from token-major keys and values (used by
+    the oracle pins) place every element where the C header's layouts say:
+    key (t, h, i) at k_pages[t / P][h][i / X][t % P][i % X], X = 16 bytes of
+    elements; value (t, h, i) at v_pages[t / P][h][i][t % P]; and the inverse
+    helpers undo them."""
+    n = 3
+    rng = np.random.default_rng(P + H + d)
+    k = rng.integers(0, 1 << 15, size=(n * P, H, d)).astype(np.int32)
+    v = rng.integers(0, 1 << 15, size=(n * P, H, d)).astype(np.int32)
+    X = wl.chunk_elems(kv_dtype)
+    kp = wl.k_tokens_to_pages(k, P, kv_dtype)
+    vp = wl.v_tokens_to_pages(v, P)
+    assert kp.shape == (n, H, d // X, P, X) and vp.shape == (n, H, d, P)
+    for t in range(n * P):
+        for h in range(H):
+            for i in range(d):
+                assert kp[t // P, h, i // X, t % P, i % X] == k[t, h, i]
+                assert vp[t // P, h, i, t % P] == v[t, h, i]
+    assert np.array_equal(wl.k_pages_to_tokens(kp), k)
+    assert np.array_equal(wl.v_pages_to_tokens(vp), v)

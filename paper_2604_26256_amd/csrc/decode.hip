@@ -108,7 +108,6 @@ __device__ __forceinline__ int desc_nvalid(uint32_t d) { return (int)(d >> 27) +
 template <int D, int P, bool FP8, int NBUF, bool SUFFIX>
 __global__ __launch_bounds__(64, 2) void decode_kernel(DecodeParams p) {
   typedef PageRegs<D, P, FP8> R;
-  constexpr int NT = R::NT;
   constexpr int KSTEPS = D / 32;
   constexpr int DBLK = D / 16;
   constexpr int E = FP8 ? 1 : 2;

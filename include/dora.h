@@ -114,12 +114,12 @@ typedef struct {
                                   only under DORA_FLAG_VALIDATE */
   uint32_t flags;              /* DORA_FLAG_* */
   int32_t num_waves;           /* decode wavefronts to launch; 0 = library
-                                  default: for fp8 pages one per resident
-                                  wavefront slot of the current device (compute
-                                  units x occupancy), for bf16 pages at most 5
-                                  per compute unit; never more than the batch
-                                  can use (B x Hkv x stride page-heads over the
-                                  minimum range) */
+                                  default: per compute unit of the current
+                                  device at most 4 for bf16 pages and 7 for
+                                  fp8 pages, within the resident wavefront
+                                  slots; never more than the batch can use
+                                  (B x Hkv x stride page-heads over the minimum
+                                  range) */
   int32_t min_range_pages;     /* smallest work range per wavefront, in
                                   (page, KV head) units; 0 = library default */
 } dora_decode_desc;

@@ -50,12 +50,14 @@ int min_range_of(const dora_decode_desc& d) {
 namespace dora {
 
 // Decode wavefronts per launch.  bf16 pages take at most kBf16WavesPerCu per
-// CU: past about one wavefront per SIMD the kernel is bound by HBM, and each
-// extra wavefront only adds cuts, partials and combine work (the 7B-class
-// batch is 2-3% faster per step at 5 per CU than at every resident slot; the larger
-// batches are level).  fp8 pages keep every resident slot: their per-page
-// conversion work needs the occupancy.  Never more than the batch can use:
-// at most B * Hkv * stride page-heads, min_range each.
+// CU, one per SIMD: past that the kernel is bound by HBM, and each extra
+// wavefront only adds cuts, partials and combine work (4 per CU against 5:
+// 1.2-1.8% faster per step on every bf16 batch; 4.5 per CU, which leaves
+// some SIMDs two wavefronts and others one, is slower than both).  fp8 pages
+// take at most kFp8WavesPerCu: their per-page conversion work needs the
+// occupancy (4 per CU: 20% slower), and 7 per CU is 0.7% faster per step than
+// every resident slot (8).  Never more than the batch can use: at most
+// B * Hkv * stride page-heads, min_range each.
 int64_t decode_waves(const dora_decode_desc& d) {
   if (d.num_waves > 0) return d.num_waves;
   int dev = 0, cus = 0, per_cu = 0;
@@ -69,7 +71,8 @@ int64_t decode_waves(const dora_decode_desc& d) {
     cus = 256;
     per_cu = 8;
   }
-  if (!fp8 && per_cu > kBf16WavesPerCu) per_cu = kBf16WavesPerCu;
+  const int cap = fp8 ? kFp8WavesPerCu : kBf16WavesPerCu;
+  if (per_cu > cap) per_cu = cap;
   const int64_t slots = (int64_t)cus * per_cu;
   const int64_t most = (int64_t)seqs * d.num_kv_heads * d.block_table_stride;
   const int64_t need = (most + min_range_of(d) - 1) / min_range_of(d);

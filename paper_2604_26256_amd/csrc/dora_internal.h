@@ -10,9 +10,10 @@
 
 namespace dora {
 
-// Decode wavefronts per compute unit for bf16 pages, at most (fp8 pages use
-// every resident slot).  One equal range per wavefront.
-constexpr int kBf16WavesPerCu = 5;
+// Decode wavefronts per compute unit, at most, for bf16 and for fp8 pages (and
+// never more than the resident slots).  One equal range per wavefront.
+constexpr int kBf16WavesPerCu = 4;
+constexpr int kFp8WavesPerCu = 7;
 // Smallest range (page-heads) a wavefront gets by default: a range must carry
 // enough bytes to amortise the wavefront's start-up (page prefix, first loads).
 constexpr int kMinRangePages = 8;

@@ -19,8 +19,9 @@
 namespace dora {
 
 // DORA_NOALLOC_WORKSPACE_BYTES: the largest decode workspace of any supported
-// geometry at the library's default launch on a 256-CU part (2,048
-// wavefronts, group 16, head_dim 128: 34.1 MB), with headroom.
+// geometry at the library's default launch on a 256-CU part (1,792
+// wavefronts, group 16, head_dim 128: 29.9 MB), with headroom for parts with
+// more compute units or a larger caller-set wavefront count.
 constexpr size_t kScratchBytes = DORA_NOALLOC_WORKSPACE_BYTES;
 constexpr int kMaxDevices = 64;
 

@@ -250,16 +250,17 @@ def test_pool_migration_rules(d):
 def test_num_waves_query(d):
     """The wave count the workspace is sized for: the caller's num_waves when
     set; otherwise no more than the batch can use (B * Hkv * stride page-heads
-    over the 8-page minimum range) and at most 5 per CU for bf16 pages (with
-    no device here the library assumes 256 CUs at 8 waves each)."""
+    over the 8-page minimum range) and at most 4 per CU for bf16 pages and 7
+    for fp8 pages (with no device here the library assumes 256 CUs at 8
+    resident waves each)."""
     assert d.dora_decode_num_waves(_desc(d, num_waves=77)) == 77
     small = _desc(d, num_seqs=2, num_kv_heads=2, num_q_heads=4, block_table_stride=8)
     assert d.dora_decode_num_waves(small) == 2 * 2 * 8 // 8
     assert d.dora_decode_num_waves(_desc(d, min_range_pages=1, num_seqs=2, num_kv_heads=2,
                                          num_q_heads=4, block_table_stride=8)) == 32
     big = d.dora_decode_num_waves(_desc(d, num_seqs=4000))
-    assert 0 < big <= 256 * 5
-    assert d.dora_decode_num_waves(_desc(d, num_seqs=4000, kv_dtype=1)) >= big
+    assert big == 256 * 4
+    assert d.dora_decode_num_waves(_desc(d, num_seqs=4000, kv_dtype=1)) == 256 * 7
     assert d.dora_decode_num_waves(_desc(d, head_dim=96)) == 0
 
 

@@ -32,6 +32,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -184,9 +185,11 @@ def summarize_trace(d, workload, grpo=False):
 
 
 def _kernel_instance(w):
-    """Template instance of the decode kernel that workload w launches."""
-    return (f"decode_kernel<{w.head_dim}, {w.page_size}, "
-            f"{'true' if w.kv_dtype == 1 else 'false'}, 3, false>")
+    """Pattern of the decode kernel's template instance that workload w
+    launches (head dim, page size, fp8 or not, the page-buffer count the
+    library picks for that geometry, plain rather than suffix decode)."""
+    return (rf"decode_kernel<{w.head_dim}, {w.page_size}, "
+            rf"{'true' if w.kv_dtype == 1 else 'false'}, \d+, false>")
 
 
 def summarize_bench_trace(d, line_path):
@@ -218,13 +221,13 @@ def summarize_bench_trace(d, line_path):
              "the same run reports for each workload launching that instance.", "",
              "| kernel instance | workloads | calls | trace avg us | event avg us | events / trace |",
              "|---|---|---|---|---|---|"]
-    for inst, names in by_inst.items():
-        hit = [(k, v) for k, v in stats.items() if inst in k]
+    for pat, names in by_inst.items():
+        hit = [(m.group(0), v) for k, v in stats.items() for m in [re.search(pat, k)] if m]
         if not hit:
             continue
-        calls, tavg = hit[0][1]
+        inst, (calls, tavg) = hit[0]
         ev = [line["workloads"][n]["roofline"]["avg_launch_ms"] * 1e3 for n in names]
-        shown = names + (["grpo7b (plain path)"] if inst in shared_with_grpo else [])
+        shown = names + (["grpo7b (plain path)"] if pat in shared_with_grpo else [])
         if len(shown) == 1:
             ratio = f"{ev[0] / tavg:.3f}"
         else:

@@ -650,11 +650,14 @@ __global__ void fill_i32_kernel(int32_t* dst, int32_t value, int64_t n) {
 // launchers
 // ---------------------------------------------------------------------------
 
-// Register buffers per wave: two pages in flight where the register budget
-// keeps two waves per SIMD, one page otherwise.
+// Register buffers per wave (NBUF - 1 pages in flight).  32-token pages of
+// head dim 128 keep one page in flight: for bf16 the register budget of two
+// waves per SIMD allows no more; for fp8 one page was 0.2-0.3% faster per
+// step than two (MoE batch, two boxes) with 190 instead of 224 registers.
+// The other geometries keep two.
 template <int D, int P, bool FP8>
 constexpr int page_buffers() {
-  return (P == 32 && !FP8 && D == 128) ? 2 : 3;
+  return (P == 32 && D == 128) ? 2 : 3;
 }
 
 template <int D, int P, bool FP8>

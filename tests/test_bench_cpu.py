@@ -146,7 +146,7 @@ def test_bench_trace_sets_trace_beside_events(tmp_path, monkeypatch):
     with open(d / "run_kernel_stats.csv", "w", newline="") as f:
         w = csv.DictWriter(f, fieldnames=["Name", "Calls", "AverageNs", "MinNs", "MaxNs"])
         w.writeheader()
-        w.writerow({"Name": "void dora::decode_kernel<128, 32, true, 3, false>(dora::DecodeParams)",
+        w.writerow({"Name": "void dora::decode_kernel<128, 32, true, 2, false>(dora::DecodeParams)",
                     "Calls": 65, "AverageNs": 2000000.0, "MinNs": 1, "MaxNs": 2})
         w.writerow({"Name": "void dora::decode_kernel<128, 16, false, 3, false>(dora::DecodeParams)",
                     "Calls": 260, "AverageNs": 100000.0, "MinNs": 1, "MaxNs": 2})
@@ -157,7 +157,7 @@ def test_bench_trace_sets_trace_beside_events(tmp_path, monkeypatch):
     (tmp_path / "line.json").write_text("[bench] noise\n" + json.dumps(line) + "\n")
     bench.summarize_bench_trace(str(d), str(tmp_path / "line.json"))
     text = open(os.path.join(bench.PROFILES, f"decode_kernel_{bench.MAIN_WORKLOAD}_bench_trace.md")).read()
-    assert "| `decode_kernel<128, 32, true, 3, false>` | moe_fp8 | 65 | 2000.00 | 2020.00 | 1.010 |" in text
+    assert "| `decode_kernel<128, 32, true, 2, false>` | moe_fp8 | 65 | 2000.00 | 2020.00 | 1.010 |" in text
     assert "rollout7b, tail_only" in text and "(shared instance)" in text
     assert bench.BENCH_TRACE_CMD in text
 

@@ -199,3 +199,45 @@ def test_append_full_size_workload_sampled(idx):
         assert np.array_equal(b.v_scales[idx_t].cpu().numpy(), hvs)
     del b
     torch.cuda.empty_cache()
+
+
+def test_append_random_geometries_bit_exact():
+    """24 seeded random geometries (dtype, page size, 1-8 KV heads, head dim,
+    1-12 sequences, 1 to 2P+3 appends, three spreads of token magnitude):
+    pages and fp8 scales bit-exact against the oracle after every run."""
+    rng = np.random.default_rng(424242)
+    D = lib()
+    for case in range(24):
+        dt = int(rng.integers(0, 2))
+        P = int(rng.choice([16, 32]))
+        Hkv = int(rng.integers(1, 9))
+        d = int(rng.choice([64, 128]))
+        B = int(rng.integers(1, 13))
+        steps = int(rng.integers(1, 2 * P + 4))
+        spread = float(rng.choice([0.3, 0.8, 2.0]))
+        print(f"[case {case}] append dt={dt} P={P} Hkv={Hkv} d={d} B={B} steps={steps} "
+              f"spread={spread}", flush=True)
+        start, bt, k, v, ks, vs, kn, vn = _setup(B, Hkv, d, P, dt, steps, seed=500 + case,
+                                                 spread=spread)
+        hk, hv = _np_codes(k, dt).copy(), _np_codes(v, dt).copy()
+        hks = None if ks is None else ks.numpy().copy()
+        hvs = None if vs is None else vs.numpy().copy()
+        d_k, d_v = k.cuda(), v.cuda()
+        d_ks = None if ks is None else ks.cuda()
+        d_vs = None if vs is None else vs.cuda()
+        d_bt = torch.from_numpy(bt).cuda()
+        status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+        for s in range(steps):
+            lens = (start + s + 1).astype(np.int32)
+            assert oracle.kv_append(_np_codes(kn[s], 0), _np_codes(vn[s], 0), bt, lens, hk, hv,
+                                    kv_dtype=dt, page_size=P, k_scales=hks, v_scales=hvs) == 0
+            D.dora_kv_append(kn[s].cuda(), vn[s].cuda(), d_bt, torch.from_numpy(lens).cuda(),
+                             d_k, d_v, num_kv_heads=Hkv, page_size=P, kv_dtype=dt,
+                             k_scales=d_ks, v_scales=d_vs, dev_status=status)
+            assert int(status.item()) == 0, (case, s)
+        torch.cuda.synchronize()
+        assert np.array_equal(_np_codes(d_k.cpu(), dt), hk), case
+        assert np.array_equal(_np_codes(d_v.cpu(), dt), hv), case
+        if dt == 1:
+            assert np.array_equal(d_ks.cpu().numpy().view(np.uint32), hks.view(np.uint32)), case
+            assert np.array_equal(d_vs.cpu().numpy().view(np.uint32), hvs.view(np.uint32)), case

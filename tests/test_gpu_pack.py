@@ -279,3 +279,61 @@ def test_pack_multi_version_workload_32_seqs():
     _assert_pools_equal_oracle(dst_k, dst_v, None, None, expected)
     del b, dst_k, dst_v
     torch.cuda.empty_cache()
+
+
+def test_pack_unpack_random_geometries_bit_exact():
+    """20 seeded random geometries (dtype, page size, 1-8 KV heads, head dim,
+    1-12 sequences of random lengths, the page list in a random order, pages
+    unpacked to random distinct ids of a pool of random bytes): the packed
+    buffer equals oracle.pack byte for byte, and the destination pool after
+    the unpack equals oracle.unpack's."""
+    d = lib()
+    rng = np.random.default_rng(9090)
+    for case in range(20):
+        dt = int(rng.integers(0, 2))
+        P = int(rng.choice([16, 32]))
+        Hkv = int(rng.integers(1, 9))
+        D = int(rng.choice([64, 128]))
+        B = int(rng.integers(1, 13))
+        lens = rng.integers(1, 1500, B).astype(np.int32)
+        n = wl.pages_needed(lens, P)
+        nb = int(n.sum()) * 2 + 16
+        print(f"[case {case}] pack/unpack dt={dt} P={P} Hkv={Hkv} d={D} B={B} pages={n.sum()}",
+              flush=True)
+        w = wl.Workload("pr", B, Hkv, Hkv, D, P, dt, nb, "uniform", lo=1, hi=1)
+        b = gpu_batch(w, lengths=lens, seed_index=3000 + case)
+        src = np.concatenate([b.block_table_h[i, :n[i]] for i in range(B)]).astype(np.int32)
+        src = src[rng.permutation(len(src))]
+        version = int(rng.integers(0, 3))
+        packed = _pack(b, src, version)
+        ks_h = None if dt == 0 else b.k_scales.cpu().numpy()
+        vs_h = None if dt == 0 else b.v_scales.cpu().numpy()
+        ref = oracle.pack(_host_codes(b.k_pages), _host_codes(b.v_pages), src, kv_dtype=dt,
+                          page_size=P, num_kv_heads=Hkv, head_dim=D, policy_version=version,
+                          n_seqs=3, k_scales=ks_h, v_scales=vs_h)
+        assert np.array_equal(packed.cpu().numpy(), ref), case
+        g = torch.Generator(device="cuda").manual_seed(7000 + case)
+        dst_k = torch.randint(0, 256, (b.k_pages.numel() * b.k_pages.element_size(),),
+                              generator=g, device="cuda", dtype=torch.uint8)
+        dst_v = torch.randint(0, 256, (b.v_pages.numel() * b.v_pages.element_size(),),
+                              generator=g, device="cuda", dtype=torch.uint8)
+        dst_k = dst_k.view(b.k_pages.dtype).view(b.k_pages.shape)
+        dst_v = dst_v.view(b.v_pages.dtype).view(b.v_pages.shape)
+        dst_ks = dst_vs = None
+        if dt:
+            dst_ks = torch.rand(nb, generator=g, device="cuda", dtype=torch.float32)
+            dst_vs = torch.rand(nb, generator=g, device="cuda", dtype=torch.float32)
+        dst_pages = rng.permutation(nb)[:len(src)].astype(np.int32)
+        expected = _oracle_unpack_expected(
+            _host_pool(packed), dst_pages, _host_pool(dst_k), _host_pool(dst_v),
+            None if dst_ks is None else _host_pool(dst_ks),
+            None if dst_vs is None else _host_pool(dst_vs), dt=dt, P=P, Hkv=Hkv, d=D,
+            version=version)
+        status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+        d.dora_kv_page_unpack(packed, torch.from_numpy(dst_pages).cuda(), dst_k, dst_v,
+                              src_version=version, num_kv_heads=Hkv, page_size=P, head_dim=D,
+                              kv_dtype=dt, policy_version=version, k_scales=dst_ks,
+                              v_scales=dst_vs, dev_status=status)
+        torch.cuda.synchronize()
+        assert status.item() == d.DORA_OK, case
+        _assert_pools_equal_oracle(dst_k, dst_v, dst_ks, dst_vs, expected)

@@ -159,3 +159,33 @@ def test_grouped_validate_flag():
     with pytest.raises(d.DoraError) as e:
         _grouped(b, 4, flags=d.DORA_FLAG_VALIDATE, page_owner=b.page_owner)
     assert e.value.status == d.DORA_ERR_DEVICE_CHECK
+
+
+def test_grouped_random_geometries():
+    """16 seeded random GRPO-shaped batches (dtype, page size, head dim, 1-4
+    KV heads, group size M and query group G with M x G <= 128, 1-3 groups,
+    prompt lengths and response mixes drawn per case): the detected shared
+    prefix equals the prompt's full pages, and the grouped output matches
+    the oracle and the plain decode within the decode tolerance."""
+    rng = np.random.default_rng(5150)
+    for case in range(16):
+        dt = int(rng.integers(0, 2))
+        P = int(rng.choice([16, 32]))
+        d = int(rng.choice([64, 128]))
+        Hkv = int(rng.integers(1, 5))
+        M = int(rng.choice([2, 3, 4, 8, 16]))
+        G = int(rng.integers(1, 128 // M + 1)) if M > 8 else int(rng.integers(1, 17))
+        G = min(G, 16, 128 // M)
+        groups = int(rng.integers(1, 4))
+        lo = int(rng.integers(P + 1, 600))
+        hi = lo + int(rng.integers(1, 1500))
+        print(f"[case {case}] grouped dt={dt} P={P} d={d} Hkv={Hkv} G={G} M={M} "
+              f"groups={groups} prompts=({lo},{hi})", flush=True)
+        w = wl.Workload("gr", groups * M, G * Hkv, Hkv, d, P, dt, 8192, "lognormal", 200, 1.0,
+                        1, 2500)
+        b, shared = wl.make_grpo_batch(w, group_size=M, prompt_range=(lo, hi), device="cuda",
+                                       seed_index=4000 + case)
+        out, det = _grouped(b, M)
+        assert det.tolist() == shared[::M].tolist(), case
+        assert max_abs_err(out, oracle_for(b)) <= TOL[dt], case
+        assert (out.float() - run_decode(b).float()).abs().max().item() <= TOL[dt], case

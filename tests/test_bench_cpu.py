@@ -3,7 +3,10 @@ bench.py reports is the decode kernel's FETCH_SIZE and WRITE_SIZE counters,
 each scaled by what the same counter reads for a copy of known size.  These
 tests feed synthetic counter files through the summary and check the
 calibration pick and the scaling against hand-computed values, and do the
-same for the compute-side counter summary (busy fractions, per-step counts)."""
+same for the compute-side counter summary (busy fractions, per-step counts),
+the roofline object (bytes per launch over the kernel's average time) and the
+per-workload rates, and the rule that a counter summary is used only on the
+kernel sources it was taken on."""
 import csv
 import json
 import os
@@ -185,3 +188,55 @@ def test_source_hash_ignores_comments_only():
     code = "int f(int x) { // add one\n  return x + 1; /* done */ }\n"
     assert bench._code_only(code) == bench._code_only("int f(int x) {\n return x + 1;  }")
     assert bench._code_only(code) != bench._code_only("int f(int x) { return x + 2; }")
+
+
+def test_roofline_object_is_bytes_over_the_kernel_average():
+    """roofline.frac is the workload's algorithmic bytes per launch over the
+    decode kernel's average event time, over the 8 TB/s peak; the two
+    reference fractions divide the same rate by the references."""
+    rec = {"algorithmic_bytes": {"total": 18_000_000_000}, "split_kernel_ms": 2.5,
+           "split_kernel_traffic_bytes": 18_300_000_000, "split_kernel_l2_hit_rate": 0.3,
+           "pattern_reference": {"best_gbps": 6_000.0}}
+    r = bench.roofline_of(rec, achievable_gbps=6_500.0)
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert r["achieved"] == pytest.approx(7_200.0)             # 18 GB / 2.5 ms
+    assert r["frac"] == pytest.approx(0.9)
+    assert r["frac_of_achievable"] == pytest.approx(7_200.0 / 6_500.0)
+    assert r["frac_of_pattern"] == pytest.approx(1.2)
+    assert r["traffic"] == 18_300_000_000 and r["avg_launch_ms"] == 2.5
+    rec.pop("pattern_reference")
+    assert bench.roofline_of(rec, 6_500.0)["frac_of_pattern"] is None
+
+
+def test_decode_record_rates_follow_the_step_times():
+    w = wl.BY_NAME["tiny"]
+    lengths = wl.sample_lengths(w, wl.seeds(0)[0])
+    ab = wl.algorithmic_bytes(w, lengths)["total"]
+    t = {"step_ms": np.array([0.010, 0.012, 0.014]), "split_ms": np.array([0.008, 0.008]),
+         "combine_ms": np.array([0.002, 0.004])}
+    r = bench.decode_record(w, lengths, t)
+    assert r["ms_per_step"] == pytest.approx(0.012)
+    assert r["decode_tokens_per_s"] == pytest.approx(w.num_seqs / 12e-6)
+    assert r["hbm_gbps"] == pytest.approx(ab / 12e-6 / 1e9)
+    assert r["hbm_frac_of_peak"] == pytest.approx(ab / 12e-6 / 1e9 / 8000.0)
+    assert r["split_kernel_gbps"] == pytest.approx(ab / 8e-6 / 1e9)
+    assert r["combine_ms"] == pytest.approx(0.003)
+    assert r["ms_p10_p50_p90"][1] == pytest.approx(0.012)
+
+
+def test_counter_summaries_are_used_only_on_matching_sources(tmp_path, monkeypatch):
+    """A committed counter summary feeds `traffic` only while the kernel
+    sources hash to the value it records, and only for its own workload."""
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    w = wl.BY_NAME["rollout7b"]
+    path = bench.pmc_path(w.name)
+    json.dump({"workload": w.name, "kernel_source_hash": bench.kernel_source_hash()},
+              open(path, "w"))
+    assert bench.load_pmc(w) is not None
+    json.dump({"workload": w.name, "kernel_source_hash": "0" * 16}, open(path, "w"))
+    assert bench.load_pmc(w) is None
+    json.dump({"workload": "tail_only", "kernel_source_hash": bench.kernel_source_hash()},
+              open(path, "w"))
+    assert bench.load_pmc(w) is None
+    os.remove(path)
+    assert bench.load_pmc(w) is None

@@ -116,3 +116,21 @@ def test_page_layout_helpers_follow_the_documented_layout(kv_dtype, P, H, d):
                 assert vp[t // P, h, i, t % P] == v[t, h, i]
     assert np.array_equal(wl.k_pages_to_tokens(kp), k)
     assert np.array_equal(wl.v_pages_to_tokens(vp), v)
+
+
+def test_algorithmic_bytes_by_hand():
+    """The roofline numerator on a case computed by hand: K and V of valid
+    tokens only (no tail slots), fp8 page scales, Q and the output, one
+    block-table entry per page and one length per sequence."""
+    w = wl.Workload("h", 3, 8, 2, 64, 16, 0, 64, "uniform", lo=1, hi=1)
+    ab = wl.algorithmic_bytes(w, np.array([17, 0, 32], np.int32))
+    assert ab["kv"] == (17 + 0 + 32) * 2 * 64 * 2 * 2      # tokens x Hkv x d x (K, V) x 2 B
+    assert ab["scales"] == 0
+    assert ab["q_out"] == 2 * 3 * 8 * 64 * 2              # Q and out, bf16
+    assert ab["meta"] == (2 + 0 + 2) * 4 + 3 * 4          # table entries, lengths
+    assert ab["total"] == ab["kv"] + ab["q_out"] + ab["meta"]
+    w8 = wl.Workload("h8", 3, 8, 2, 64, 32, 1, 64, "uniform", lo=1, hi=1)
+    ab8 = wl.algorithmic_bytes(w8, np.array([17, 0, 33], np.int32))
+    assert ab8["kv"] == (17 + 33) * 2 * 64 * 2 * 1          # fp8: one byte per element
+    assert ab8["scales"] == (1 + 0 + 2) * 2 * 4             # fp32 K and V scale per page
+    assert ab8["meta"] == (1 + 0 + 2) * 4 + 3 * 4

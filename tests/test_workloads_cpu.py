@@ -134,3 +134,17 @@ def test_algorithmic_bytes_by_hand():
     assert ab8["kv"] == (17 + 33) * 2 * 64 * 2 * 1          # fp8: one byte per element
     assert ab8["scales"] == (1 + 0 + 2) * 2 * 4             # fp32 K and V scale per page
     assert ab8["meta"] == (1 + 0 + 2) * 4 + 3 * 4
+
+
+def test_shared_prefix_bytes_count_shared_pages_once_per_group():
+    """Grouped accounting: every member but the group's first has its shared
+    pages' K and V subtracted once; table entries are still read per member."""
+    w = wl.Workload("g", 4, 8, 2, 64, 16, 0, 64, "uniform", lo=1, hi=1)
+    lengths = np.array([100, 90, 50, 60], np.int32)
+    shared = np.array([5, 5, 3, 3], np.int32)          # groups of two
+    plain = wl.algorithmic_bytes(w, lengths)
+    g = wl.shared_prefix_algorithmic_bytes(w, lengths, shared, 2)
+    dup = (5 + 3) * 16 * 2 * 64 * 2 * 2                 # members 1 and 3: pages x P x Hkv x d x (K, V) x 2 B
+    assert g["duplicate_kv_not_counted"] == dup
+    assert g["kv"] == plain["kv"] - dup and g["total"] == plain["total"] - dup
+    assert g["meta"] == plain["meta"]

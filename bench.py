@@ -107,7 +107,7 @@ def log(msg):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=MAIN_WORKLOAD, choices=[w.name for w in wl.WORKLOADS])
     ap.add_argument("--only-main", action="store_true", help="skip the other workloads")

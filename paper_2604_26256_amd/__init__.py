@@ -7,6 +7,7 @@ before the library exists.
 """
 _EXPORTS = (
     "DORA_FLAG_VALIDATE", "DORA_KV_BF16", "DORA_KV_FP8_E4M3", "DoraError", "Pool",
+    "PreparedDecode",
     "dora_decode_attn", "dora_decode_attn_grouped", "dora_decode_workspace_bytes",
     "dora_kv_append", "dora_kv_packed_bytes", "dora_kv_page_pack", "dora_kv_page_unpack",
     "make_decode_desc", "make_pack_desc", "plan_partition", "plan_supplement",

@@ -341,6 +341,62 @@ def dora_decode_attn(q, k_pages, v_pages, block_table, seq_lens, version_ids, ou
     return out
 
 
+class PreparedDecode:
+    """dora_decode_attn with its arguments checked and marshalled once, for
+    host loops that call the same batch buffers step after step.
+
+    Takes the arguments of dora_decode_attn and checks them as it does; a call
+    of the object then runs only the C call, so it costs the C ABI's own host
+    time, a fraction of what dora_decode_attn spends checking every tensor on
+    every call.  The object keeps references to the tensors and
+    their device addresses: refill q, block_table, seq_lens, version_ids (and
+    the pages and scales) in place between calls, on the same stream or
+    ordered before it; new tensors need a new object.  Geometry, flags and
+    the stream (default: the current stream when the object is made) are
+    fixed.  It owns a workspace of its own (or uses the one given), so calls
+    of different objects never share one; calls of one object are ordered by
+    its stream.  Returns `out` from each call."""
+
+    def __init__(self, q, k_pages, v_pages, block_table, seq_lens, version_ids, out, *,
+                 num_kv_heads: int, page_size: int, kv_dtype: int = DORA_KV_BF16,
+                 sm_scale: float = 0.0, k_scales=None, v_scales=None, page_owner=None,
+                 flags: int = 0, num_waves: int = 0, min_range_pages: int = 0,
+                 workspace=None, stream=None):
+        torch = _torch()
+        self.out = out
+        self._keep = (q, k_pages, v_pages, block_table, seq_lens, version_ids, out, k_scales,
+                      v_scales, page_owner)
+        self._desc, args = _decode_args(
+            q, k_pages, v_pages, block_table, seq_lens, version_ids, out,
+            num_kv_heads=num_kv_heads, page_size=page_size, kv_dtype=kv_dtype,
+            sm_scale=sm_scale, k_scales=k_scales, v_scales=v_scales, page_owner=page_owner,
+            flags=flags, num_waves=num_waves, min_range_pages=min_range_pages)
+        self._args = None
+        if args is None:  # empty batch: every call is a no-op
+            return
+        s = stream if stream is not None else torch.cuda.current_stream(q.device)
+        handle = ctypes.c_void_p(s.cuda_stream)
+        need = dora_decode_workspace_bytes(self._desc)
+        if need == 0:  # invalid or unsupported geometry: let the library name the reason
+            _check(_lib.dora_decode_attn(ctypes.byref(self._desc), *args, None, 0, handle),
+                   "dora_decode_attn")
+        if workspace is None:
+            with torch.cuda.stream(s):
+                workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        elif workspace.numel() < need:
+            raise ValueError(f"workspace: {workspace.numel()} bytes, {need} needed")
+        self.workspace = workspace
+        ws_ptr = _dev_ptr(workspace, "workspace", (torch.uint8,))
+        self._args = (ctypes.byref(self._desc), *args, ws_ptr, workspace.numel(), handle)
+
+    def __call__(self):
+        if self._args is not None:
+            st = _lib.dora_decode_attn(*self._args)
+            if st != DORA_OK:
+                raise DoraError(st, "dora_decode_attn")
+        return self.out
+
+
 NOALLOC_WORKSPACE_BYTES = 48 << 20   # DORA_NOALLOC_WORKSPACE_BYTES
 
 

@@ -115,3 +115,43 @@ def test_stream_read_empty_list_and_bad_args():
                            tile_bytes=3000)
     assert e.value.status == d.DORA_ERR_UNSUPPORTED
 
+
+
+@pytest.mark.parametrize("kv_dtype", [0, 1])
+def test_prepared_decode_follows_in_place_updates(kv_dtype):
+    """A prepared call gives, bit for bit, what dora_decode_attn gives on the
+    same buffers, also after the queries and lengths are refilled in place
+    (lengths anywhere from 0 to their pages' capacity), and matches the
+    oracle on the last refill."""
+    print(f"[case] prepared decode kv_dtype={kv_dtype}", flush=True)
+    from gpu_util import max_abs_err, oracle_for
+    d = lib()
+    P = 16 if kv_dtype == 0 else 32
+    w = wl.Workload("p", 24, 16, 2, 128, P, kv_dtype, 8192, "lognormal", 600, 1.0, 16, 4000)
+    b = gpu_batch(w, seed_index=71, poison=False)
+    kw = dict(num_kv_heads=w.num_kv_heads, page_size=w.page_size, kv_dtype=w.kv_dtype,
+              k_scales=b.k_scales, v_scales=b.v_scales)
+    out = torch.empty_like(b.q)
+    prep = d.PreparedDecode(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens,
+                            b.version_ids, out, **kw)
+    capacity = ((b.lengths + P - 1) // P) * P  # tokens the sequences' pages hold
+    rng = np.random.default_rng(71)
+    gen = torch.Generator(device="cuda").manual_seed(71)
+    for step in range(4):
+        if step:
+            b.q.copy_(torch.randn(b.q.shape, generator=gen, device="cuda").to(torch.bfloat16))
+            b.lengths = rng.integers(0, capacity + 1).astype(np.int32)
+            b.lengths[0] = 0
+            b.seq_lens.copy_(torch.from_numpy(b.lengths).cuda())
+        ref = torch.empty_like(b.q)
+        d.dora_decode_attn(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens,
+                           b.version_ids, ref, **kw)
+        assert prep() is out
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), step
+    err = max_abs_err(out, oracle_for(b))
+    print(f"[case] prepared decode: max-abs err {err:.3e}", flush=True)
+    assert err <= (2e-2 if kv_dtype == 0 else 5e-2)
+    empty = d.PreparedDecode(b.q[:0], b.k_pages, b.v_pages, b.block_table[:0], b.seq_lens[:0],
+                             b.version_ids[:0], out[:0], **kw)
+    assert empty().numel() == 0

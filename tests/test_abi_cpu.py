@@ -312,3 +312,27 @@ def test_noalloc_entry_refuses_before_any_launch(d):
             full = _desc(d, num_seqs=8192, num_q_heads=128, num_kv_heads=8, head_dim=hd,
                          kv_dtype=dt, block_table_stride=4096)
             assert 0 < d.dora_decode_workspace_bytes(full) <= d.NOALLOC_WORKSPACE_BYTES
+
+
+def test_prepared_decode_checks_arguments_like_the_plain_call(d):
+    """The prepared call runs the plain call's checks when it is made: host
+    tensors, wrong dtypes and wrong page shapes are refused before anything
+    reaches the library; an empty batch is a no-op."""
+    import torch
+    B, Hq, Hkv, D, P, n = 3, 8, 2, 128, 16, 32
+    q = torch.zeros(B, Hq, D, dtype=torch.bfloat16)
+    k = torch.zeros(n, Hkv, D // 8, P, 8, dtype=torch.bfloat16)
+    v = torch.zeros(n, Hkv, D, P, dtype=torch.bfloat16)
+    bt = torch.zeros(B, 4, dtype=torch.int32)
+    lens = torch.ones(B, dtype=torch.int32)
+    out = torch.empty_like(q)
+    kw = dict(num_kv_heads=Hkv, page_size=P)
+    for fn in (d.dora_decode_attn, d.PreparedDecode):
+        with pytest.raises(ValueError, match="on the GPU"):
+            fn(q, k, v, bt, lens, None, out, **kw)
+        with pytest.raises(ValueError, match="v_pages must be"):
+            fn(q, k, v[:, :, :64], bt, lens, None, out, **kw)
+        with pytest.raises(ValueError, match="k_pages must be"):
+            fn(q, k, v, bt, lens, None, out, num_kv_heads=Hkv, page_size=32)
+    empty = d.PreparedDecode(q[:0], k, v, bt[:0], lens[:0], None, out[:0], **kw)
+    assert empty() is not None and empty().numel() == 0

@@ -777,7 +777,10 @@ def cpu_baseline(b, budget_s=20.0, min_s=10.0, threads=None):
                   probe["seq_lens"], num_kv_heads=b.w.num_kv_heads, page_size=b.w.page_size,
                   kv_dtype=b.w.kv_dtype, k_scales=probe["k_scales"],
                   v_scales=probe["v_scales"], num_pages=probe["num_pages"], nthreads=cores)
-    per_tok = (time.perf_counter() - t0) / max(1, int(b.lengths[0]))
+    # the probe is one sequence, so at most Hkv of the threads had work: its
+    # wall time times that count is its CPU time
+    busy = min(cores, b.w.num_kv_heads)
+    per_tok = (time.perf_counter() - t0) * busy / max(1, int(b.lengths[0]))
     take, acc = [], 0.0
     for s in order:
         take.append(s)
